@@ -1,0 +1,250 @@
+// Span metadata, tied position ids, rotary embedding and decode-step commit.
+//
+// Span metadata follows Section 3.1 (sentinel tokens around a span; <CL>
+// visible only to itself; enclosed tokens hidden from tokens after the <CR>)
+// and the position tie of Section 3.1 "Input Transformation".
+#include <math.h>
+
+#include <cmath>
+#include <cstring>
+#include <vector>
+
+#include "sckv_common.h"
+
+namespace sckv {
+
+// ---------------------------------------------------------------------------
+// vu[t] and tied positions: one workgroup per sequence, 256 threads.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void span_meta_kernel(const int32_t* __restrict__ spans,
+                                                        const int32_t* __restrict__ nspan,
+                                                        int32_t b, int32_t s_max, int32_t L_meta,
+                                                        int32_t* __restrict__ vu,
+                                                        int32_t* __restrict__ pos) {
+  const int s = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6;
+  const int32_t* cl = spans + (int64_t)s * s_max;
+  const int32_t* cr = spans + (int64_t)b * s_max + (int64_t)s * s_max;
+  const int n = nspan[s];
+  __shared__ int wave_cnt[4];
+  int carry = 0;
+  for (int base = 0; base < L_meta; base += 256) {
+    const int t = base + tid;
+    bool normal = false;
+    int v = SCKV_INF_VU;
+    if (t < L_meta) {
+      // last span whose <CL> is at or before t
+      int lo = 0, hi = n;  // answer in [lo-1, hi-1]
+      while (lo < hi) {
+        int mid = (lo + hi) >> 1;
+        if (cl[mid] <= t) lo = mid + 1; else hi = mid;
+      }
+      const int k = lo - 1;
+      if (k >= 0 && t == cl[k]) {
+        v = t;                          // <CL>
+      } else if (k >= 0 && t < cr[k]) {
+        v = cr[k];                      // enclosed token
+        normal = true;
+      } else if (k >= 0 && t == cr[k]) {
+        v = SCKV_INF_VU;                // <CR>
+      } else {
+        normal = true;                  // plain normal token
+      }
+      vu[(int64_t)s * L_meta + t] = v;
+    }
+    const uint64_t m = __ballot(normal);
+    const int rank = mask_rank(m);
+    if ((tid & 63) == 0) wave_cnt[wave] = __popcll(m);
+    __syncthreads();
+    int off = carry, total = 0;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const int c = wave_cnt[w];
+      if (w < wave) off += c;
+      total += c;
+    }
+    if (pos != nullptr && t < L_meta) {
+      const int before = off + rank;  // normal tokens in [0, t)
+      pos[(int64_t)s * L_meta + t] = normal ? before : (before > 0 ? before - 1 : 0);
+    }
+    carry += total;
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// rotary embedding, rotate-half form: pair (i, i + d/2) turns by
+// pos * theta^(-2i/d).  One thread per 16-byte piece of the first half.
+// ---------------------------------------------------------------------------
+struct InvFreq {
+  double w[64];
+};
+
+template <typename T, int D>
+__global__ __launch_bounds__(256) void rope_kernel(const T* x, T* y,
+                                                   int32_t H, int32_t n, int64_t xs, int64_t ys,
+                                                   const int32_t* __restrict__ pos, int32_t L_meta,
+                                                   int32_t tok0, int64_t total, InvFreq inv,
+                                                   int rotate) {
+  constexpr int E = Piece<T>::E;
+  constexpr int HALF = D / 2;
+  constexpr int PPH = HALF / E;  // pieces per half row
+  static_assert(HALF % E == 0, "half row must be whole pieces");
+  const double two_pi = 6.283185307179586476925286766559;
+  for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; g < total;
+       g += (int64_t)gridDim.x * blockDim.x) {
+    const int p = (int)(g % PPH);
+    const int64_t rowg = g / PPH;  // (s*H + h)*n + t
+    const int t = (int)(rowg % n);
+    const int64_t bh = rowg / n;
+    const int s = (int)(bh / H);
+    const T* src = x + bh * xs + (int64_t)t * D;
+    T* dst = y + bh * ys + (int64_t)t * D;
+    u32x4 a = ld16(src + p * E), c = ld16(src + HALF + p * E);
+    if (rotate) {
+      float fa[E], fc[E];
+      Piece<T>::unpack(a, fa);
+      Piece<T>::unpack(c, fc);
+      const double ps = (double)pos[(int64_t)s * L_meta + tok0 + t];
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        double ang = ps * inv.w[p * E + e];
+        ang -= two_pi * rint(ang / two_pi);
+        float sn, cs;
+        sincosf((float)ang, &sn, &cs);
+        const float x1 = fa[e], x2 = fc[e];
+        fa[e] = x1 * cs - x2 * sn;
+        fc[e] = x2 * cs + x1 * sn;
+      }
+      a = Piece<T>::pack(fa);
+      c = Piece<T>::pack(fc);
+    }
+    st16(dst + p * E, a);
+    st16(dst + HALF + p * E, c);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// decode-step commit: one thread per sequence
+// ---------------------------------------------------------------------------
+__global__ void commit_kernel(int32_t* __restrict__ kv_len, int32_t* __restrict__ tok_idx,
+                              int32_t* __restrict__ pos_ids, int32_t* __restrict__ cur_tok,
+                              const int32_t* __restrict__ vu, const int32_t* __restrict__ pos,
+                              int32_t L_meta, int32_t b, int32_t L_cap, int32_t* status) {
+  const int s = blockIdx.x * blockDim.x + threadIdx.x;
+  if (s >= b) return;
+  const int t = cur_tok[s];
+  if (t < 0 || t >= L_meta) {
+    if (status) atomicOr(status, SCKV_STATUS_TOKEN);
+  } else if (vu[(int64_t)s * L_meta + t] != t) {
+    const int n = kv_len[s];
+    if (n < 0 || n >= L_cap) {
+      if (status) atomicOr(status, SCKV_STATUS_CAP);
+    } else {
+      tok_idx[(int64_t)s * L_cap + n] = t;
+      pos_ids[(int64_t)s * L_cap + n] = pos[(int64_t)s * L_meta + t];
+      kv_len[s] = n + 1;
+    }
+  }
+  cur_tok[s] = t + 1;
+}
+
+}  // namespace sckv
+
+using namespace sckv;
+
+extern "C" int sckv_span_meta(const int32_t* cl_host, const int32_t* cr_host,
+                              const int32_t* n_host, int32_t s_max, int32_t b, int32_t L_meta,
+                              int32_t* spans_dev, int32_t* vu, int32_t* pos, hipStream_t stream) {
+  clear_error();
+  if (!cl_host || !cr_host || !n_host || !spans_dev || !vu)
+    return fail(SCKV_EINVAL, "sckv_span_meta: null pointer");
+  if (b <= 0 || s_max <= 0 || L_meta <= 0)
+    return fail(SCKV_EINVAL, "sckv_span_meta: b, s_max and L_meta must be positive");
+  for (int s = 0; s < b; ++s) {
+    const int n = n_host[s];
+    if (n < 0 || n > s_max)
+      return fail(SCKV_ESPAN, "sckv_span_meta: span count of sequence " + std::to_string(s) +
+                                  " outside [0, s_max]");
+    for (int k = 0; k < n; ++k) {
+      const int32_t c = cl_host[(int64_t)s * s_max + k], r = cr_host[(int64_t)s * s_max + k];
+      if (c < 0 || c >= L_meta || r <= c)
+        return fail(SCKV_ESPAN, "sckv_span_meta: sequence " + std::to_string(s) + " span " +
+                                    std::to_string(k) + " needs 0 <= cl < L_meta and cl < cr");
+      if (k > 0 && c <= cr_host[(int64_t)s * s_max + k - 1])
+        return fail(SCKV_ESPAN, "sckv_span_meta: sequence " + std::to_string(s) + " span " +
+                                    std::to_string(k) + " overlaps or is out of order");
+    }
+  }
+  // Pack [cl | cr | n] and copy it in one transfer.  The source is a
+  // pageable host vector: the copy has consumed it when the call returns.
+  std::vector<int32_t> packed((size_t)2 * b * s_max + b);
+  std::memcpy(packed.data(), cl_host, (size_t)b * s_max * sizeof(int32_t));
+  std::memcpy(packed.data() + (size_t)b * s_max, cr_host, (size_t)b * s_max * sizeof(int32_t));
+  std::memcpy(packed.data() + (size_t)2 * b * s_max, n_host, (size_t)b * sizeof(int32_t));
+  int rc = hip_check(hipMemcpyAsync(spans_dev, packed.data(), packed.size() * sizeof(int32_t),
+                                    hipMemcpyHostToDevice, stream),
+                     "sckv_span_meta: span upload");
+  if (rc) return rc;
+  span_meta_kernel<<<b, 256, 0, stream>>>(spans_dev, spans_dev + (size_t)2 * b * s_max, b, s_max,
+                                          L_meta, vu, pos);
+  return hip_check(hipGetLastError(), "sckv_span_meta: launch");
+}
+
+template <typename T, int D>
+static int launch_rope(const void* x, void* y, int32_t b, int32_t H, int32_t n, int64_t xs,
+                       int64_t ys, const int32_t* pos, int32_t L_meta, int32_t tok0, float theta,
+                       hipStream_t stream) {
+  InvFreq inv;
+  for (int i = 0; i < 64; ++i) inv.w[i] = 0.0;
+  for (int i = 0; i < D / 2; ++i) inv.w[i] = std::pow((double)theta, -2.0 * i / D);
+  constexpr int PPH = D / 2 / Piece<T>::E;
+  const int64_t total = (int64_t)b * H * n * PPH;
+  int64_t blocks = (total + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  rope_kernel<T, D><<<(unsigned)blocks, 256, 0, stream>>>(
+      static_cast<const T*>(x), static_cast<T*>(y), H, n, xs, ys, pos, L_meta, tok0, total, inv,
+      theta > 0.f ? 1 : 0);
+  return hip_check(hipGetLastError(), "rope_apply: launch");
+}
+
+extern "C" int rope_apply(const void* x, void* y, int32_t b, int32_t H, int32_t n,
+                          int64_t x_stride_bh, int64_t y_stride_bh, int32_t d_head, sckv_dtype dt,
+                          const int32_t* pos, int32_t L_meta, int32_t tok0, float theta,
+                          hipStream_t stream) {
+  clear_error();
+  if (!x || !y) return fail(SCKV_EINVAL, "rope_apply: null pointer");
+  if (!valid_dtype(dt)) return fail(SCKV_EINVAL, "rope_apply: unknown dtype");
+  if (!supported_d(d_head)) return fail(SCKV_EUNSUP, "rope_apply: d_head must be 64 or 80");
+  if (b <= 0 || H <= 0 || n < 0) return fail(SCKV_EINVAL, "rope_apply: bad sizes");
+  if (x_stride_bh < (int64_t)n * d_head || y_stride_bh < (int64_t)n * d_head)
+    return fail(SCKV_EINVAL, "rope_apply: slice stride smaller than n*d_head");
+  if (!(theta >= 0.f) || std::isinf(theta)) return fail(SCKV_EINVAL, "rope_apply: theta must be finite and >= 0");
+  if (theta > 0.f) {
+    if (!pos) return fail(SCKV_EINVAL, "rope_apply: null pos");
+    if (tok0 < 0 || L_meta <= 0 || (int64_t)tok0 + n > L_meta)
+      return fail(SCKV_EINVAL, "rope_apply: rows [tok0, tok0+n) exceed L_meta");
+  }
+  if (!aligned16(x) || !aligned16(y) || (x_stride_bh * elem_bytes(dt)) % 16 ||
+      (y_stride_bh * elem_bytes(dt)) % 16)
+    return fail(SCKV_EINVAL, "rope_apply: buffers and strides must be 16-byte aligned");
+  if (n == 0) return SCKV_OK;
+  if (dt == SCKV_BF16)
+    return d_head == 64 ? launch_rope<uint16_t, 64>(x, y, b, H, n, x_stride_bh, y_stride_bh, pos, L_meta, tok0, theta, stream)
+                        : launch_rope<uint16_t, 80>(x, y, b, H, n, x_stride_bh, y_stride_bh, pos, L_meta, tok0, theta, stream);
+  return d_head == 64 ? launch_rope<float, 64>(x, y, b, H, n, x_stride_bh, y_stride_bh, pos, L_meta, tok0, theta, stream)
+                      : launch_rope<float, 80>(x, y, b, H, n, x_stride_bh, y_stride_bh, pos, L_meta, tok0, theta, stream);
+}
+
+extern "C" int kv_commit(int32_t* kv_len, int32_t* tok_idx, int32_t* pos_ids, int32_t* cur_tok,
+                         const int32_t* vu, const int32_t* pos, int32_t L_meta, int32_t b,
+                         int32_t L_cap, int32_t* status, hipStream_t stream) {
+  clear_error();
+  if (!kv_len || !tok_idx || !pos_ids || !cur_tok || !vu || !pos)
+    return fail(SCKV_EINVAL, "kv_commit: null pointer");
+  if (b <= 0 || L_cap <= 0 || L_meta <= 0) return fail(SCKV_EINVAL, "kv_commit: bad sizes");
+  commit_kernel<<<(b + 255) / 256, 256, 0, stream>>>(kv_len, tok_idx, pos_ids, cur_tok, vu, pos,
+                                                     L_meta, b, L_cap, status);
+  return hip_check(hipGetLastError(), "kv_commit: launch");
+}

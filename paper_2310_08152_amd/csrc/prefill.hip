@@ -1,0 +1,475 @@
+// Causal attention under the <CL>/<CR> span-exclusion mask (prefill).
+// Section 1 (tokens after a <CR> do not attend to the tokens its span
+// encloses) and Section 3.1 (<CL> attends only to itself; normal tokens attend
+// to earlier <CR> and normal tokens).
+//
+// With vu[] as in sckv.h, row i may attend to column j iff
+//   j <= i <= vu[j]  and  (vu[i] != i or j == i).
+//
+// plan kernel: for every (sequence, 128-row query block [I, I+128)) the list
+//   of key columns j < I+128 with vu[j] >= I, i.e. the columns at least one
+//   row of the block may see, in ascending order, packed as
+//   j | min(vu[j]-I, 255) << 24.  Columns hidden from the whole block (closed
+//   spans, <CL>s before the block) are not in the list and are never read.
+// main kernel: one workgroup per (sequence, head, query block), 4 waves of 32
+//   query rows.  Key/value rows named by the list are gathered 64 at a time
+//   into LDS (double buffered for bf16); S^T = K Q^T and O^T += V^T P^T run
+//   on 32x32 MFMA tiles (bf16 inputs, fp32 accumulation; fp32 inputs use the
+//   fp32 MFMA), with an online softmax per query held in the lane that owns
+//   the query's column.  Element masks are applied only on tiles that are
+//   not entirely visible to a wave; a tile entirely in a wave's future is
+//   skipped.  A <CL> row's output is its own value row (it sees only itself),
+//   written directly in the epilogue.
+#include <math.h>
+
+#include <cmath>
+#include <type_traits>
+
+#include "sckv_common.h"
+
+namespace sckv {
+
+constexpr int PF_BQ = 128;
+constexpr int PF_BK = 64;
+constexpr int PF_THREADS = 256;
+constexpr uint32_t PF_NONE = 0x00ffffffu;  // list entry of a padding column
+constexpr float PF_LOG2E = 1.4426950408889634f;
+
+__global__ __launch_bounds__(256) void prefill_plan_kernel(const int32_t* __restrict__ vu,
+                                                           int32_t L_meta, int32_t L, int32_t n_qt,
+                                                           int32_t L_pad,
+                                                           uint32_t* __restrict__ list,
+                                                           int32_t* __restrict__ count) {
+  const int qt = blockIdx.x;
+  const int s = blockIdx.y;
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6;
+  const int I = qt * PF_BQ;
+  const int jend = min(I + PF_BQ, L);
+  const int32_t* v = vu + (int64_t)s * L_meta;
+  uint32_t* out = list + ((int64_t)s * n_qt + qt) * L_pad;
+  __shared__ int wave_cnt[4];
+  int carry = 0;
+  for (int base = 0; base < jend; base += 256) {
+    const int j = base + tid;
+    bool ok = false;
+    uint32_t e = 0;
+    if (j < jend) {
+      const int x = v[j];
+      ok = x >= I;
+      const int64_t rel = (int64_t)x - I;
+      e = (uint32_t)j | ((uint32_t)(rel > 255 ? 255 : rel) << 24);
+    }
+    const uint64_t m = __ballot(ok);
+    if ((tid & 63) == 0) wave_cnt[wave] = __popcll(m);
+    __syncthreads();
+    int off = carry, total = 0;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const int c = wave_cnt[w];
+      if (w < wave) off += c;
+      total += c;
+    }
+    if (ok) out[off + mask_rank(m)] = e;
+    carry += total;
+    __syncthreads();
+  }
+  if (tid == 0) count[(int64_t)s * n_qt + qt] = carry;
+}
+
+// ---------------------------------------------------------------------------
+// tile geometry per element type
+// ---------------------------------------------------------------------------
+template <typename T, int D> struct PfCfg;
+
+template <int D> struct PfCfg<uint16_t, D> {
+  static constexpr int NBUF = 2;
+  static constexpr int DP = (D + 31) / 32 * 32;     // value rows padded to whole 32-row MFMA blocks
+  static constexpr int KP = D + 8;                  // K tile: [64][KP] bf16
+  static constexpr int VP = PF_BK + 4;              // V^T tile: [DP][VP] bf16
+  static constexpr int KBYTES = PF_BK * KP * 2;
+  static constexpr int VBYTES = DP * VP * 2;
+  static constexpr int PPR = D / 8;                 // 16-byte pieces per row
+  static constexpr int KSTEPS = D / 16;
+};
+
+template <int D> struct PfCfg<float, D> {
+  static constexpr int NBUF = 1;
+  static constexpr int DP = (D + 31) / 32 * 32;
+  static constexpr int KP = D + 2;                  // K tile: [64][KP] f32
+  static constexpr int VP = DP + 8;                 // V tile: [64][VP] f32 (row-major)
+  static constexpr int KBYTES = PF_BK * KP * 4;
+  static constexpr int VBYTES = PF_BK * VP * 4;
+  static constexpr int PPR = D / 4;
+  static constexpr int KSTEPS = D / 2;
+};
+
+struct TileInfo {
+  int jmin, jmax, vrmin, nvalid;
+};
+
+template <typename T, int D>
+struct PfSmem {
+  using C = PfCfg<T, D>;
+  char k[C::NBUF][C::KBYTES];
+  char v[C::NBUF][C::VBYTES];
+  uint32_t ent[C::NBUF][PF_BK];
+  TileInfo info[C::NBUF];
+};
+
+// ---------------------------------------------------------------------------
+// main kernel
+// ---------------------------------------------------------------------------
+template <typename T, int D>
+__global__ __launch_bounds__(PF_THREADS, 2) void prefill_attn_kernel(
+    const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v, T* __restrict__ o,
+    int32_t H, int32_t L, int64_t qs, int64_t kvs, int64_t os, float c2,
+    const int32_t* __restrict__ vu, int32_t L_meta, const uint32_t* __restrict__ list,
+    const int32_t* __restrict__ count, int32_t n_qt, int32_t L_pad, int32_t n_work) {
+  using C = PfCfg<T, D>;
+  constexpr bool BF = sizeof(T) == 2;
+  constexpr int PPR = C::PPR;
+  constexpr int NPIECE = PF_BK * PPR;                       // pieces per K (or V) tile
+  constexpr int PPT = (NPIECE + PF_THREADS - 1) / PF_THREADS;  // pieces per thread
+  constexpr int NDB = C::DP / 32;                           // output d blocks
+
+  __shared__ PfSmem<T, D> sm;
+
+  // XCD-aware work order: consecutive work items (same (sequence, head),
+  // heaviest query block first) land on the same XCD and share its L2.
+  const int x = blockIdx.x;
+  const int xcd = x & 7, idx = x >> 3;
+  const int qn = n_work >> 3, rem = n_work & 7;
+  const int work = xcd * qn + min(xcd, rem) + idx;
+  const int bh = work / n_qt;
+  const int qt = n_qt - 1 - (work % n_qt);
+  const int s = bh / H;
+  const int I = qt * PF_BQ;
+
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6;
+  const int lane = tid & 63;
+  const int l32 = lane & 31;
+  const int g = lane >> 5;
+  const int Iw = I + wave * 32;
+  const int qrow = Iw + l32;
+  const bool wave_live = Iw < L;
+
+  const T* qb = q + (int64_t)bh * qs;
+  const T* kb = k + (int64_t)bh * kvs;
+  const T* vb = v + (int64_t)bh * kvs;
+  const uint32_t* ents = list + ((int64_t)s * n_qt + qt) * L_pad;
+  const int n_vis = count[(int64_t)s * n_qt + qt];
+  const int nt = (n_vis + PF_BK - 1) / PF_BK;
+
+  // zero the padding value rows/columns once (never written afterwards)
+  if constexpr (C::DP != D) {
+    for (int b = 0; b < C::NBUF; ++b) {
+      if constexpr (BF) {
+        uint16_t* vt = reinterpret_cast<uint16_t*>(sm.v[b]);
+        for (int i = tid; i < (C::DP - D) * C::VP; i += PF_THREADS) vt[D * C::VP + i] = 0;
+      } else {
+        float* vs = reinterpret_cast<float*>(sm.v[b]);
+        for (int i = tid; i < PF_BK * (C::DP - D); i += PF_THREADS)
+          vs[(i / (C::DP - D)) * C::VP + D + i % (C::DP - D)] = 0.f;
+      }
+    }
+  }
+
+  // Q^T operand, held for the whole kernel
+  using QReg = typename std::conditional<BF, bf16x8, float>::type;
+  QReg qreg[C::KSTEPS];
+#pragma unroll
+  for (int kk = 0; kk < C::KSTEPS; ++kk) {
+    if constexpr (BF) {
+      u32x4 w = qrow < L ? ld16(qb + (int64_t)qrow * D + kk * 16 + g * 8) : u32x4{0, 0, 0, 0};
+      qreg[kk] = __builtin_bit_cast(bf16x8, w);
+    } else {
+      qreg[kk] = qrow < L ? qb[(int64_t)qrow * D + 2 * kk + g] : 0.f;
+    }
+  }
+
+  f32x16 oacc[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) oacc[db][i] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+
+  // ---- staging of one gathered tile: global -> registers -> LDS ----
+  u32x4 kreg[PPT], vreg[PPT];
+  uint32_t ereg = PF_NONE;
+  auto load_tile = [&](int kt) {
+    const int base = kt * PF_BK;
+    const int nvalid = min(PF_BK, n_vis - base);
+#pragma unroll
+    for (int p = 0; p < PPT; ++p) {
+      const int piece = p * PF_THREADS + tid;
+      const int r = piece / PPR, sg = piece % PPR;
+      kreg[p] = u32x4{0, 0, 0, 0};
+      vreg[p] = u32x4{0, 0, 0, 0};
+      if (piece < NPIECE && r < nvalid) {
+        const int j = (int)(ents[base + r] & 0x00ffffffu);
+        kreg[p] = ld16(kb + (int64_t)j * D + sg * Piece<T>::E);
+        vreg[p] = ld16(vb + (int64_t)j * D + sg * Piece<T>::E);
+      }
+    }
+    ereg = (tid < nvalid) ? ents[base + tid] : PF_NONE;
+  };
+  auto store_tile = [&](int kt, int buf) {
+    const int base = kt * PF_BK;
+    const int nvalid = min(PF_BK, n_vis - base);
+#pragma unroll
+    for (int p = 0; p < PPT; ++p) {
+      const int piece = p * PF_THREADS + tid;
+      if (piece >= NPIECE) continue;
+      const int r = piece / PPR, sg = piece % PPR;
+      if constexpr (BF) {
+        *reinterpret_cast<u32x4*>(sm.k[buf] + (r * C::KP + sg * 8) * 2) = kreg[p];
+        uint16_t* vt = reinterpret_cast<uint16_t*>(sm.v[buf]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          vt[(sg * 8 + 2 * e) * C::VP + r] = (uint16_t)(vreg[p][e] & 0xffffu);
+          vt[(sg * 8 + 2 * e + 1) * C::VP + r] = (uint16_t)(vreg[p][e] >> 16);
+        }
+      } else {
+        float* ks = reinterpret_cast<float*>(sm.k[buf]) + r * C::KP + sg * 4;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) ks[e] = __uint_as_float(kreg[p][e]);
+        *reinterpret_cast<u32x4*>(sm.v[buf] + (r * C::VP + sg * 4) * 4) = vreg[p];
+      }
+    }
+    if (tid < 64) {
+      sm.ent[buf][tid] = ereg;
+      int vr = (tid < nvalid) ? (int)(ereg >> 24) : 255;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) vr = min(vr, __shfl_xor(vr, off, 64));
+      if (tid == 0) {
+        TileInfo ti;
+        ti.jmin = (int)(ereg & 0x00ffffffu);
+        ti.jmax = (int)(ents[base + nvalid - 1] & 0x00ffffffu);
+        ti.vrmin = vr;
+        ti.nvalid = nvalid;
+        sm.info[buf] = ti;
+      }
+    }
+  };
+
+  load_tile(0);
+  store_tile(0, 0);
+  __syncthreads();
+
+  for (int kt = 0; kt < nt; ++kt) {
+    const int cur = kt % C::NBUF;
+    if (kt + 1 < nt) load_tile(kt + 1);
+
+    const TileInfo ti = sm.info[cur];
+    if (wave_live && ti.jmin <= Iw + 31) {
+      const bool full = ti.nvalid == PF_BK && ti.jmax <= Iw && ti.vrmin >= Iw + 31 - I;
+      // ---- S^T = K Q^T for the two 32-key blocks ----
+      f32x16 sacc[2];
+#pragma unroll
+      for (int kb2 = 0; kb2 < 2; ++kb2) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) sacc[kb2][i] = 0.f;
+        if constexpr (BF) {
+          const char* krow = sm.k[cur] + ((kb2 * 32 + l32) * C::KP + g * 8) * 2;
+#pragma unroll
+          for (int kk = 0; kk < C::KSTEPS; ++kk) {
+            const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(krow + kk * 32));
+            sacc[kb2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[kk], sacc[kb2], 0, 0, 0);
+          }
+        } else {
+          const float* krow = reinterpret_cast<const float*>(sm.k[cur]) + (kb2 * 32 + l32) * C::KP + g;
+#pragma unroll
+          for (int kk = 0; kk < C::KSTEPS; ++kk)
+            sacc[kb2] = __builtin_amdgcn_mfma_f32_32x32x2f32(krow[2 * kk], qreg[kk], sacc[kb2], 0, 0, 0);
+        }
+      }
+      // ---- element mask on tiles not entirely visible to this wave ----
+      if (!full) {
+        const int ir = qrow - I;
+#pragma unroll
+        for (int kb2 = 0; kb2 < 2; ++kb2)
+#pragma unroll
+          for (int vv = 0; vv < 16; ++vv) {
+            const int key = kb2 * 32 + 8 * (vv >> 2) + 4 * g + (vv & 3);
+            const uint32_t e = sm.ent[cur][key];
+            const int j = (int)(e & 0x00ffffffu);
+            const int vr = (int)(e >> 24);
+            if (!(j <= qrow && ir <= vr)) sacc[kb2][vv] = -INFINITY;
+          }
+      }
+      // ---- online softmax (log2 units) ----
+      float mx = -INFINITY;
+#pragma unroll
+      for (int kb2 = 0; kb2 < 2; ++kb2)
+#pragma unroll
+        for (int vv = 0; vv < 16; ++vv) mx = fmaxf(mx, sacc[kb2][vv]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float m_new = fmaxf(m_run, mx * c2);
+      const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+      const float alpha = exp2f(m_run - m_use);
+      float rs = 0.f;
+#pragma unroll
+      for (int kb2 = 0; kb2 < 2; ++kb2)
+#pragma unroll
+        for (int vv = 0; vv < 16; ++vv) {
+          const float p = exp2f(fmaf(sacc[kb2][vv], c2, -m_use));
+          sacc[kb2][vv] = p;
+          rs += p;
+        }
+      l_run = l_run * alpha + rs;
+      m_run = m_new;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
+      // ---- O^T += V^T P^T ----
+      if constexpr (BF) {
+        bf16x8 pb[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          u32x4 w;
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            w[i] = pack_bf16x2(sacc[t >> 1][8 * (t & 1) + 2 * i], sacc[t >> 1][8 * (t & 1) + 2 * i + 1]);
+          pb[t] = __builtin_bit_cast(bf16x8, w);
+        }
+        const uint16_t* vt = reinterpret_cast<const uint16_t*>(sm.v[cur]);
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) {
+          const uint16_t* vrow = vt + (db * 32 + l32) * C::VP + 4 * g;
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            const u32x2 lo = *reinterpret_cast<const u32x2*>(vrow + 16 * t);
+            const u32x2 hi = *reinterpret_cast<const u32x2*>(vrow + 16 * t + 8);
+            const u32x4 w = u32x4{lo[0], lo[1], hi[0], hi[1]};
+            oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, w), pb[t],
+                                                               oacc[db], 0, 0, 0);
+          }
+        }
+      } else {
+        const float* vs = reinterpret_cast<const float*>(sm.v[cur]);
+#pragma unroll
+        for (int db = 0; db < NDB; ++db)
+#pragma unroll
+          for (int kb2 = 0; kb2 < 2; ++kb2)
+#pragma unroll
+            for (int vv = 0; vv < 16; ++vv) {
+              const int key = kb2 * 32 + 8 * (vv >> 2) + 4 * g + (vv & 3);
+              oacc[db] = __builtin_amdgcn_mfma_f32_32x32x2f32(vs[key * C::VP + db * 32 + l32],
+                                                              sacc[kb2][vv], oacc[db], 0, 0, 0);
+            }
+      }
+    }
+
+    if constexpr (C::NBUF == 1) __syncthreads();
+    if (kt + 1 < nt) store_tile(kt + 1, (kt + 1) % C::NBUF);
+    __syncthreads();
+  }
+
+  // ---- epilogue: normalise and write; a <CL> row copies its value row ----
+  if (!wave_live) return;
+  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+  if (qrow >= L) return;
+  const float inv = 1.f / l_tot;
+  const bool is_cl = vu[(int64_t)s * L_meta + qrow] == qrow;
+  T* orow = o + (int64_t)bh * os + (int64_t)qrow * D;
+  const T* vrow = vb + (int64_t)qrow * D;
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      const int d0 = db * 32 + 8 * jj + 4 * g;
+      if (d0 >= D) continue;
+      if constexpr (BF) {
+        u32x2 w;
+        if (is_cl) {
+          w = *reinterpret_cast<const u32x2*>(vrow + d0);
+        } else {
+          w[0] = pack_bf16x2(oacc[db][4 * jj] * inv, oacc[db][4 * jj + 1] * inv);
+          w[1] = pack_bf16x2(oacc[db][4 * jj + 2] * inv, oacc[db][4 * jj + 3] * inv);
+        }
+        *reinterpret_cast<u32x2*>(orow + d0) = w;
+      } else {
+        u32x4 w;
+        if (is_cl) {
+          w = ld16(vrow + d0);
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) w[i] = __float_as_uint(oacc[db][4 * jj + i] * inv);
+        }
+        st16(orow + d0, w);
+      }
+    }
+}
+
+template <typename T, int D>
+static int launch_prefill(const void* q, const void* k, const void* v, void* o, int32_t b,
+                          int32_t H, int32_t L, int64_t qs, int64_t kvs, int64_t os, float scale,
+                          const int32_t* vu, int32_t L_meta, uint32_t* list, int32_t* count,
+                          int32_t n_qt, int32_t L_pad, hipStream_t stream) {
+  prefill_plan_kernel<<<dim3(n_qt, b), 256, 0, stream>>>(vu, L_meta, L, n_qt, L_pad, list, count);
+  int rc = hip_check(hipGetLastError(), "span_masked_prefill_attn: plan launch");
+  if (rc) return rc;
+  const int n_work = b * H * n_qt;
+  prefill_attn_kernel<T, D><<<n_work, PF_THREADS, 0, stream>>>(
+      static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
+      static_cast<T*>(o), H, L, qs, kvs, os, scale * PF_LOG2E, vu, L_meta, list, count, n_qt,
+      L_pad, n_work);
+  return hip_check(hipGetLastError(), "span_masked_prefill_attn: launch");
+}
+
+static void plan_geometry(int32_t L, int32_t* n_qt, int32_t* L_pad) {
+  *n_qt = (L + PF_BQ - 1) / PF_BQ;
+  *L_pad = *n_qt * PF_BQ;
+}
+
+}  // namespace sckv
+
+using namespace sckv;
+
+extern "C" size_t sckv_prefill_workspace_bytes(int32_t b, int32_t L) {
+  if (b <= 0 || L <= 0) return 0;
+  int32_t n_qt, L_pad;
+  plan_geometry(L, &n_qt, &L_pad);
+  const size_t list = (size_t)b * n_qt * L_pad * sizeof(uint32_t);
+  const size_t cnt = ((size_t)b * n_qt * sizeof(int32_t) + 255) / 256 * 256;
+  return list + cnt;
+}
+
+extern "C" int span_masked_prefill_attn(const void* q, const void* k, const void* v, void* o,
+                                        int32_t b, int32_t H, int32_t L, int32_t d_head,
+                                        int64_t q_stride_bh, int64_t kv_stride_bh,
+                                        int64_t o_stride_bh, sckv_dtype dt, float scale,
+                                        const int32_t* vu, int32_t L_meta, void* ws,
+                                        size_t ws_bytes, hipStream_t stream) {
+  clear_error();
+  if (!q || !k || !v || !o || !vu || !ws) return fail(SCKV_EINVAL, "span_masked_prefill_attn: null pointer");
+  if (!valid_dtype(dt)) return fail(SCKV_EINVAL, "span_masked_prefill_attn: unknown dtype");
+  if (!supported_d(d_head)) return fail(SCKV_EUNSUP, "span_masked_prefill_attn: d_head must be 64 or 80");
+  if (b <= 0 || H <= 0 || L <= 0) return fail(SCKV_EINVAL, "span_masked_prefill_attn: sizes must be positive");
+  if (L > 32768) return fail(SCKV_EUNSUP, "span_masked_prefill_attn: L above 32768");
+  if (L_meta < L) return fail(SCKV_EINVAL, "span_masked_prefill_attn: L_meta < L");
+  const int64_t rowlen = (int64_t)L * d_head;
+  if (q_stride_bh < rowlen || kv_stride_bh < rowlen || o_stride_bh < rowlen)
+    return fail(SCKV_EINVAL, "span_masked_prefill_attn: slice stride smaller than L*d_head");
+  const int eb = elem_bytes(dt);
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(ws) ||
+      (q_stride_bh * eb) % 16 || (kv_stride_bh * eb) % 16 || (o_stride_bh * eb) % 16)
+    return fail(SCKV_EINVAL, "span_masked_prefill_attn: buffers and strides must be 16-byte aligned");
+  if (!(scale > 0.f) || std::isinf(scale)) return fail(SCKV_EINVAL, "span_masked_prefill_attn: scale must be finite and > 0");
+  if (ws_bytes < sckv_prefill_workspace_bytes(b, L))
+    return fail(SCKV_EINVAL, "span_masked_prefill_attn: workspace too small");
+  int32_t n_qt, L_pad;
+  plan_geometry(L, &n_qt, &L_pad);
+  if ((int64_t)b * H * n_qt > 0x7fffffff) return fail(SCKV_EUNSUP, "span_masked_prefill_attn: grid too large");
+  uint32_t* list = static_cast<uint32_t*>(ws);
+  int32_t* cnt = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + (size_t)b * n_qt * L_pad * sizeof(uint32_t));
+  if (dt == SCKV_BF16)
+    return d_head == 64 ? launch_prefill<uint16_t, 64>(q, k, v, o, b, H, L, q_stride_bh, kv_stride_bh, o_stride_bh, scale, vu, L_meta, list, cnt, n_qt, L_pad, stream)
+                        : launch_prefill<uint16_t, 80>(q, k, v, o, b, H, L, q_stride_bh, kv_stride_bh, o_stride_bh, scale, vu, L_meta, list, cnt, n_qt, L_pad, stream);
+  return d_head == 64 ? launch_prefill<float, 64>(q, k, v, o, b, H, L, q_stride_bh, kv_stride_bh, o_stride_bh, scale, vu, L_meta, list, cnt, n_qt, L_pad, stream)
+                      : launch_prefill<float, 80>(q, k, v, o, b, H, L, q_stride_bh, kv_stride_bh, o_stride_bh, scale, vu, L_meta, list, cnt, n_qt, L_pad, stream);
+}

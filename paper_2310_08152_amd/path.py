@@ -1,0 +1,109 @@
+"""Host-side orchestration of the hot path: buffer allocation (torch, device
+memory only) and the order of C-ABI calls.  No arithmetic of the method is
+done here; every step runs in libsckv.so kernels.
+
+Typical use (one batch of sequences):
+    meta  = SpanMeta(spans, L_meta, device)          # span metadata, tied positions
+    cache = KVCache(M, b, H, L_cap, d, dtype, device)
+    for m in layers: prefill_layer(...)               # rotary + masked attention
+    cache.compact(meta, next_tok)                     # free closed spans in place
+    for step: for m: decode_layer(...); commit(...)   # generate
+"""
+from __future__ import annotations
+
+import math
+from typing import List, Sequence, Tuple
+
+import torch
+
+from . import binding as B
+from .workload import spans_to_arrays
+
+
+class SpanMeta:
+    """Device span metadata (vu) and tied position ids for a batch."""
+
+    def __init__(self, spans: Sequence[Sequence[Tuple[int, int]]], L_meta: int, device,
+                 stream=None):
+        cl, cr, n = spans_to_arrays(list(spans))
+        b, s_max = cl.shape
+        self.b, self.L_meta, self.device = b, L_meta, torch.device(device)
+        self.spans_dev = torch.empty(2 * b * s_max + b, dtype=torch.int32, device=device)
+        self.vu = torch.empty(b, L_meta, dtype=torch.int32, device=device)
+        self.pos = torch.empty(b, L_meta, dtype=torch.int32, device=device)
+        B.sckv_span_meta(cl, cr, n, L_meta, self.spans_dev, self.vu, self.pos, stream=stream)
+
+
+class KVCache:
+    """(M, 2, b, H, L_cap, d) cache with per-sequence row bookkeeping."""
+
+    def __init__(self, M: int, b: int, H: int, L_cap: int, d: int, dtype, device):
+        self.M, self.b, self.H, self.L_cap, self.d = M, b, H, L_cap, d
+        self.kv = torch.empty(M, 2, b, H, L_cap, d, dtype=dtype, device=device)
+        self.kv_len = torch.zeros(b, dtype=torch.int32, device=device)
+        self.tok_idx = torch.zeros(b, L_cap, dtype=torch.int32, device=device)
+        self.pos_ids = torch.zeros(b, L_cap, dtype=torch.int32, device=device)
+        self.kept_src = torch.empty(b, L_cap, dtype=torch.int32, device=device)
+        self.cur_tok = torch.zeros(b, dtype=torch.int32, device=device)
+        self.status = torch.zeros(1, dtype=torch.int32, device=device)
+
+    def k(self, m: int):
+        return self.kv[m, 0]
+
+    def v(self, m: int):
+        return self.kv[m, 1]
+
+    def start_prompt(self, L: int, meta: SpanMeta):
+        """Rows [0, L) hold prompt tokens 0..L-1; the next token is L."""
+        self.tok_idx[:, :L] = torch.arange(L, dtype=torch.int32, device=self.kv.device)
+        self.pos_ids[:, :L] = meta.pos[:, :L]
+        self.kv_len.fill_(L)
+        self.cur_tok.fill_(L)
+
+    def compact(self, meta: SpanMeta, next_tok=None, kv_out=None, stream=None):
+        nt = self.cur_tok if next_tok is None else next_tok
+        B.kv_compact(self.kv, kv_out, self.M, self.b, self.H, self.L_cap, self.d, self.kv_len,
+                     self.tok_idx, self.pos_ids, nt, meta.vu, meta.L_meta, self.kept_src,
+                     stream=stream)
+
+    def commit(self, meta: SpanMeta, stream=None):
+        B.kv_commit(self.kv_len, self.tok_idx, self.pos_ids, self.cur_tok, meta.vu, meta.pos,
+                    meta.L_meta, self.b, self.L_cap, self.status, stream=stream)
+
+
+class Workspace:
+    """Device workspaces sized for a batch shape."""
+
+    def __init__(self, b: int, H: int, L: int, L_cap: int, d: int, device):
+        self.prefill = torch.empty(max(1, B.sckv_prefill_workspace_bytes(b, max(L, 1))),
+                                   dtype=torch.uint8, device=device)
+        self.decode = torch.empty(max(1, B.sckv_decode_workspace_bytes(b, H, L_cap, d)),
+                                  dtype=torch.uint8, device=device)
+
+
+def default_scale(d: int) -> float:
+    return 1.0 / math.sqrt(d)
+
+
+def rope_rows(x, y, meta: SpanMeta, n: int, tok0: int, theta: float, stream=None):
+    """Rotate rows [0, n) of every (b, h) slice of x (b, H, >=n, d) into y."""
+    b, H, _, d = x.shape
+    B.rope_apply(x, y, b, H, n, x.stride(1), y.stride(1), d, meta.pos, meta.L_meta, tok0, theta,
+                 stream=stream)
+
+
+def prefill_layer(q, k, v, o, meta: SpanMeta, ws: Workspace, L: int, scale=None, stream=None):
+    """Masked attention of q (b,H,L,d) over key/value slices k, v (b,H,>=L,d)."""
+    b, H, _, d = q.shape
+    B.span_masked_prefill_attn(q, k, v, o, b, H, L, d, q.stride(1), k.stride(1), o.stride(1),
+                               default_scale(d) if scale is None else scale, meta.vu,
+                               meta.L_meta, ws.prefill, stream=stream)
+
+
+def decode_layer(q, k_new, v_new, cache: KVCache, m: int, meta: SpanMeta, ws: Workspace, o,
+                 scale=None, theta: float = 0.0, stream=None):
+    d = q.shape[-1]
+    B.compacted_decode_attn(q, k_new, v_new, cache.k(m), cache.v(m), cache.kv_len, cache.cur_tok,
+                            meta.vu, meta.pos, meta.L_meta, o, cache.b, cache.H, cache.L_cap, d,
+                            default_scale(d) if scale is None else scale, theta, ws.decode,
+                            cache.status, stream=stream)

@@ -1,0 +1,140 @@
+"""The C ABI loads, exports every declared symbol, and rejects bad arguments
+on the host before any HIP call (so these run without a GPU)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sckv.h")
+
+
+@pytest.fixture(scope="module")
+def B():
+    from paper_2310_08152_amd import binding
+    return binding
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*([a-z_][a-z_0-9]*)\s*\(", text, flags=re.M)
+    return sorted(set(names))
+
+
+def test_every_declared_symbol_is_exported(B):
+    names = declared_functions()
+    assert len(names) >= 10, names
+    for n in names:
+        assert hasattr(B.lib, n), n
+        assert n in B.EXPORTS, n
+
+
+def test_version(B):
+    assert "gfx950" in B.version()
+
+
+FAKE = ctypes.c_void_p(4096)  # never dereferenced: every call below fails a host check first
+NULL = None
+
+
+def test_span_meta_rejects_bad_spans(B):
+    vu = FAKE
+    def call(cl, cr, n, L=100):
+        cl = np.asarray(cl, np.int32).reshape(1, -1)
+        cr = np.asarray(cr, np.int32).reshape(1, -1)
+        n = np.asarray([n], np.int32)
+        return B.lib.sckv_span_meta(cl.ctypes.data, cr.ctypes.data, n.ctypes.data, cl.shape[1], 1,
+                                    L, FAKE, vu, NULL, NULL)
+    assert call([5, 10], [10, 20], 2) == B.ESPAN        # cr_0 == cl_1: overlap
+    assert call([10, 5], [12, 8], 2) == B.ESPAN         # unsorted
+    assert call([5], [5], 1) == B.ESPAN                 # cl == cr
+    assert call([100], [120], 1) == B.ESPAN             # cl >= L_meta
+    assert call([-1], [3], 1) == B.ESPAN                # negative
+    assert call([1], [3], 2) == B.ESPAN                 # n > s_max
+    assert "overlap" in B.last_error() or "s_max" in B.last_error()
+    cl = np.zeros((1, 1), np.int32)
+    assert B.lib.sckv_span_meta(cl.ctypes.data, cl.ctypes.data, cl.ctypes.data, 1, 1, 10, NULL,
+                                FAKE, NULL, NULL) == B.EINVAL
+
+
+def test_prefill_rejects(B):
+    f = B.lib.span_masked_prefill_attn
+    ws = B.lib.sckv_prefill_workspace_bytes(1, 256)
+    assert ws > 0
+    ok = dict(b=1, H=4, L=256, d=64, qs=256 * 64, kvs=256 * 64, os=256 * 64, dt=B.F32, scale=0.125)
+    def call(**kw):
+        a = dict(ok, **kw)
+        return f(FAKE, FAKE, FAKE, FAKE, a["b"], a["H"], a["L"], a["d"], a["qs"], a["kvs"], a["os"],
+                 a["dt"], a["scale"], FAKE, a.get("L_meta", 256), FAKE, a.get("ws", ws), NULL)
+    assert call(d=96) == B.EUNSUP
+    assert call(dt=7) == B.EINVAL
+    assert call(L=0) == B.EINVAL
+    assert call(qs=100) == B.EINVAL
+    assert call(L_meta=255) == B.EINVAL
+    assert call(ws=ws - 1) == B.EINVAL
+    assert call(scale=0.0) == B.EINVAL
+    assert call(L=40000, qs=40000 * 64, kvs=40000 * 64, os=40000 * 64, L_meta=40000) == B.EUNSUP
+    assert f(NULL, FAKE, FAKE, FAKE, 1, 4, 256, 64, 256 * 64, 256 * 64, 256 * 64, B.F32, 0.1,
+             FAKE, 256, FAKE, ws, NULL) == B.EINVAL
+    # misaligned
+    assert f(ctypes.c_void_p(4098), FAKE, FAKE, FAKE, 1, 4, 256, 64, 256 * 64, 256 * 64, 256 * 64,
+             B.F32, 0.1, FAKE, 256, FAKE, ws, NULL) == B.EINVAL
+
+
+def test_compact_rejects(B):
+    f = B.lib.kv_compact
+    args = [FAKE, NULL, 2, 1, 4, 128, 64, B.BF16, FAKE, FAKE, FAKE, FAKE, FAKE, 128, FAKE, NULL]
+    bad_d = list(args); bad_d[6] = 72
+    assert f(*bad_d) == B.EUNSUP
+    bad_m = list(args); bad_m[2] = 0
+    assert f(*bad_m) == B.EINVAL
+    same = list(args); same[1] = FAKE
+    assert f(*same) == B.EINVAL
+    nul = list(args); nul[8] = NULL
+    assert f(*nul) == B.EINVAL
+    big = list(args); big[5] = 70000
+    assert f(*big) == B.EUNSUP
+
+
+def test_decode_rejects(B):
+    f = B.lib.compacted_decode_attn
+    ws = B.lib.sckv_decode_workspace_bytes(2, 4, 512, 80)
+    assert ws == 2 * 4 * 2 * 82 * 4
+    def call(**kw):
+        a = dict(d=80, dt=B.BF16, scale=0.1, theta=0.0, ws=ws, pos=FAKE, b=2, H=4, Lc=512)
+        a.update(kw)
+        return f(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, a["pos"], 600, FAKE, a["b"], a["H"],
+                 a["Lc"], a["d"], a["dt"], a["scale"], a["theta"], FAKE, a["ws"], NULL, NULL)
+    assert call(d=128) == B.EUNSUP
+    assert call(ws=ws - 4) == B.EINVAL
+    assert call(theta=-1.0) == B.EINVAL
+    assert call(theta=1e4, pos=NULL) == B.EINVAL
+    assert call(scale=float("nan")) == B.EINVAL
+    assert call(b=70000) == B.EUNSUP
+
+
+def test_rope_and_commit_reject(B):
+    assert B.lib.rope_apply(FAKE, FAKE, 1, 1, 10, 640, 640, 64, B.BF16, FAKE, 100, 95, 1e4,
+                            NULL) == B.EINVAL  # rows past L_meta
+    assert B.lib.rope_apply(FAKE, FAKE, 1, 1, 10, 64, 640, 64, B.BF16, FAKE, 100, 0, 1e4,
+                            NULL) == B.EINVAL  # stride
+    assert B.lib.rope_apply(FAKE, FAKE, 1, 1, 10, 640, 640, 48, B.BF16, FAKE, 100, 0, 1e4,
+                            NULL) == B.EUNSUP
+    assert B.lib.kv_commit(FAKE, FAKE, FAKE, NULL, FAKE, FAKE, 10, 1, 10, NULL, NULL) == B.EINVAL
+    assert B.lib.kv_commit(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 10, 0, 10, NULL, NULL) == B.EINVAL
+
+
+def test_workspace_sizes(B):
+    assert B.lib.sckv_prefill_workspace_bytes(0, 10) == 0
+    assert B.lib.sckv_prefill_workspace_bytes(2, 300) >= 2 * 3 * 384 * 4
+    assert B.lib.sckv_decode_workspace_bytes(1, 1, 1, 64) == 66 * 4
+
+
+def test_binding_raises_with_message(B):
+    with pytest.raises(B.SckvError) as e:
+        B.sckv_span_meta(np.array([[5, 10]]), np.array([[10, 20]]), np.array([2]), 100,
+                         None, None)
+    assert e.value.code == B.EINVAL or e.value.code == B.ESPAN

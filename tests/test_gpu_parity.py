@@ -1,0 +1,463 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle on the
+same seeded inputs.  Integer/index/byte results must match bit for bit;
+attention outputs within max-abs 2e-2 (bf16 inputs) or 1e-5 (fp32)."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import sckv_oracle as O
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+TOL = {"bf16": 2e-2, "f32": 1e-5}
+INF = 0x7fffffff
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2310_08152_amd import binding  # noqa: F401  (fails loudly without the library)
+
+
+def P():
+    from paper_2310_08152_amd import path
+    return path
+
+
+def W():
+    from paper_2310_08152_amd import workload
+    return workload
+
+
+def f64(t):
+    return t.detach().to("cpu", torch.float64).numpy()
+
+
+def rnd(shape, seed, dtype):
+    return W().randn(shape, seed=seed, dtype=dtype).to(DEV)
+
+
+def say(msg):
+    print(msg, flush=True)
+
+
+def random_spans(L, rng, max_len=40, gap=8, start_at_zero=False, open_end=False):
+    out, c = [], 0 if start_at_zero else int(rng.integers(0, gap + 1))
+    while c < L - 1:
+        r = c + int(rng.integers(1, max_len + 1))
+        if r >= L:
+            if open_end:
+                out.append((c, L + 5))
+            break
+        out.append((c, r))
+        c = r + 1 + int(rng.integers(0, gap + 1))
+    return out
+
+
+def mask_from_vu(vu):
+    L = len(vu)
+    i = np.arange(L)[:, None]
+    j = np.arange(L)[None, :]
+    cl_row = (vu == np.arange(L))[:, None]
+    return (j <= i) & (i <= vu[None, :].astype(np.int64)) & (~cl_row | (i == j))
+
+
+# ---------------------------------------------------------------------------
+# span metadata and tied positions
+# ---------------------------------------------------------------------------
+
+SPAN_CASES = {
+    "none": (lambda L, rng: [], 77),
+    "start-at-zero-adjacent": (lambda L, rng: [(0, 3), (4, 9), (10, 11), (12, 30)], 64),
+    "open-end": (lambda L, rng: [(5, 20), (40, 300)], 100),
+    "random": (lambda L, rng: random_spans(L, rng, open_end=True), 300),
+    "random-long": (lambda L, rng: random_spans(L, rng, max_len=200, gap=50), 1500),
+}
+
+
+@pytest.mark.parametrize("case", list(SPAN_CASES))
+def test_span_meta_matches_oracle(case):
+    say(f"span_meta case={case}")
+    gen, L = SPAN_CASES[case]
+    rng = np.random.default_rng(5)
+    spans = [gen(L, rng) for _ in range(3)]
+    meta = P().SpanMeta(spans, L, DEV)
+    vu = meta.vu.cpu().numpy()
+    pos = meta.pos.cpu().numpy()
+    for s, sp in enumerate(spans):
+        types = O.token_types(sp, L)
+        assert np.array_equal(pos[s], O.tie_positions(types)), s
+        if L <= 400:
+            assert np.array_equal(mask_from_vu(vu[s]), O.attention_mask(types)), s
+        for Pn in [0, 1, L // 3, L // 2, L - 1, L]:
+            keep = O.keep_rows(types, Pn)
+            gpu_keep = (vu[s] != np.arange(L)) & (vu[s].astype(np.int64) >= Pn)
+            assert np.array_equal(gpu_keep[:Pn], keep[:Pn]), (s, Pn)
+
+
+# ---------------------------------------------------------------------------
+# rotary embedding
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype,d", [("bf16", 64), ("bf16", 80), ("f32", 64), ("f32", 80)])
+def test_rope_matches_oracle(dtype, d):
+    say(f"rope dtype={dtype} d={d}")
+    L = 300
+    spans = [[(3, 40), (50, 51), (60, 200)], [(0, 10)]]
+    meta = P().SpanMeta(spans, L, DEV)
+    x = rnd((2, 3, 257, d), 11, dtype)
+    y = torch.empty_like(x)
+    P().rope_rows(x, y, meta, n=257, tok0=20, theta=10000.0)
+    z = x.clone()
+    P().rope_rows(z, z, meta, n=257, tok0=20, theta=10000.0)          # in place
+    assert torch.equal(y, z)
+    c = torch.empty_like(x)
+    P().rope_rows(x, c, meta, n=257, tok0=20, theta=0.0)              # copy
+    assert torch.equal(c, x)
+    X, Y = f64(x), f64(y)
+    for s in range(2):
+        pos = O.tie_positions(O.token_types(spans[s], L))[20:277]
+        for h in range(3):
+            ref = O.rope_rotate_half(X[s, h], pos, 10000.0)
+            err = np.abs(Y[s, h] - ref)
+            if dtype == "bf16":
+                assert (err <= 2.0 ** -8 * np.abs(ref) + 1e-3).all(), err.max()
+            else:
+                assert err.max() < 1e-5
+
+
+# ---------------------------------------------------------------------------
+# prefill
+# ---------------------------------------------------------------------------
+
+def run_prefill(q, k, v, spans, L_meta=None):
+    b, H, L, d = q.shape
+    meta = P().SpanMeta(spans, L_meta or L, DEV)
+    ws = P().Workspace(b, H, L, L, d, DEV)
+    o = torch.full_like(q, float("nan"))
+    P().prefill_layer(q, k, v, o, meta, ws, L)
+    torch.cuda.synchronize()
+    return o
+
+
+def oracle_prefill(q, k, v, spans, heads=None):
+    Q, K, V = f64(q), f64(k), f64(v)
+    b, H, L, d = Q.shape
+    out = {}
+    for s in range(b):
+        m = O.attention_mask(O.token_types(spans[s], L))
+        hs = range(H) if heads is None else [h for (ss, h) in heads if ss == s]
+        for h in hs:
+            out[(s, h)] = O.masked_attention(Q[s, h][None], K[s, h][None], V[s, h][None], m)[0]
+    return out
+
+
+PREFILL_CASES = [
+    # name, dtype, b, H, L, d, span generator
+    ("tiny-f32-config", "f32", 1, 4, 256, 64, "tiny"),
+    ("f32-d80-ragged", "f32", 1, 2, 200, 80, "random"),
+    ("bf16-d64-windows", "bf16", 2, 4, 2048, 64, "windows"),
+    ("bf16-d80-uniform-ragged", "bf16", 2, 2, 1000, 80, "uniform"),
+    ("bf16-d64-nospans", "bf16", 1, 2, 333, 64, "none"),
+    ("bf16-d64-L1", "bf16", 1, 1, 1, 64, "none"),
+    ("bf16-d64-L37-zero-start", "bf16", 1, 3, 37, 64, "zero"),
+    ("bf16-d80-L129-open", "bf16", 2, 1, 129, 80, "open"),
+    ("bf16-d64-long-spans", "bf16", 1, 2, 700, 64, "long"),
+]
+
+
+def make_spans(kind, b, L, rng):
+    w = W()
+    if kind == "tiny":
+        return [w.spans_periodic(L, 32, 8, 24) for _ in range(b)]
+    if kind == "windows":
+        return [w.spans_jittered_windows(L, 64, 16, 32, 4, rng) for _ in range(b)]
+    if kind == "uniform":
+        return [w.spans_uniform_lengths(L, 0.5, 16, 64, rng) for _ in range(b)]
+    if kind == "none":
+        return [[] for _ in range(b)]
+    if kind == "zero":
+        return [[(0, 5), (6, 7), (8, 20), (30, 50)] for _ in range(b)]
+    if kind == "open":
+        return [[(10, 60), (61, 62), (100, 150)], [(128, 140)]][:b]
+    if kind == "long":
+        return [[(5, 400), (401, 650)] for _ in range(b)]
+    return [random_spans(L, rng, open_end=True) for _ in range(b)]
+
+
+@pytest.mark.parametrize("name,dtype,b,H,L,d,kind", PREFILL_CASES, ids=[c[0] for c in PREFILL_CASES])
+def test_prefill_matches_oracle(name, dtype, b, H, L, d, kind):
+    say(f"prefill case={name} b={b} H={H} L={L} d={d} dtype={dtype}")
+    rng = np.random.default_rng(L)
+    spans = make_spans(kind, b, L, rng)
+    q, k, v = (rnd((b, H, L, d), 100 + i, dtype) for i in range(3))
+    o = run_prefill(q, k, v, spans)
+    ref = oracle_prefill(q, k, v, spans)
+    Og, V = f64(o), f64(v)
+    worst = 0.0
+    for (s, h), r in ref.items():
+        worst = max(worst, np.abs(Og[s, h] - r).max())
+        for c, _ in spans[s]:
+            if c < L:  # a <CL> row is its own value row, bit for bit
+                assert np.array_equal(Og[s, h, c], V[s, h, c]), (s, h, c)
+    assert np.isfinite(Og).all()
+    assert worst <= TOL[dtype], worst
+
+
+def test_prefill_eviction_invariance_bitexact():
+    say("prefill eviction invariance")
+    b, H, L, d = 2, 4, 1100, 64
+    rng = np.random.default_rng(9)
+    spans = make_spans("uniform", b, L, rng)
+    q, k, v = (rnd((b, H, L, d), 200 + i, "bf16") for i in range(3))
+    o1 = run_prefill(q, k, v, spans)
+    k2, v2 = k.clone(), v.clone()
+    for s in range(b):
+        for c, r in spans[s]:
+            k2[s, :, c:r] = 1e4
+            v2[s, :, c:r] = -1e4
+    o2 = run_prefill(q, k2, v2, spans)
+    for s in range(b):
+        inside = np.zeros(L, bool)
+        for c, r in spans[s]:
+            inside[c:min(r, L - 1) + 1] = True
+        rows = torch.from_numpy(np.nonzero(~inside)[0]).to(DEV)
+        assert torch.equal(o1[s][:, rows], o2[s][:, rows])
+        assert not torch.equal(o1[s], o2[s])
+
+
+def test_prefill_full_size_opt13b_sampled():
+    """The OPT-1.3B-shaped prefill slice at full size, 8 sampled heads."""
+    w = W().get_workload("opt1.3b-prefill")
+    say(f"prefill full size {w}")
+    spans = W().workload_spans(w)
+    shape = (w.batch, w.heads, w.seq_len, w.d_head)
+    q, k, v = (W().randn(shape, seed=w.seed * 10 + i, dtype="bf16", device=DEV) for i in range(3))
+    o = run_prefill(q, k, v, spans)
+    rng = np.random.default_rng(0)
+    picks = [(int(rng.integers(w.batch)), int(rng.integers(w.heads))) for _ in range(8)]
+    for s, h in picks:
+        m = O.attention_mask(O.token_types(spans[s], w.seq_len))
+        r = O.masked_attention(f64(q[s, h])[None], f64(k[s, h])[None], f64(v[s, h])[None], m)[0]
+        assert np.abs(f64(o[s, h]) - r).max() <= TOL["bf16"]
+
+
+# ---------------------------------------------------------------------------
+# compaction
+# ---------------------------------------------------------------------------
+
+def build_cache(M, b, H, L_cap, d, dtype, L, spans, seed):
+    meta = P().SpanMeta(spans, L_cap, DEV)
+    cache = P().KVCache(M, b, H, L_cap, d, W().torch_dtype(dtype), DEV)
+    cache.kv.copy_(W().randn(cache.kv.shape, seed=seed, dtype=dtype).to(DEV))
+    cache.start_prompt(L, meta)
+    return meta, cache
+
+
+def bits(t):
+    return t.view(torch.int16 if t.element_size() == 2 else torch.int32).cpu().numpy()
+
+
+@pytest.mark.parametrize("dtype,d", [("bf16", 64), ("bf16", 80), ("f32", 64), ("f32", 80)])
+def test_compaction_bitexact(dtype, d):
+    say(f"compaction dtype={dtype} d={d}")
+    M, b, H, L_cap = 2, 4, 3, 600
+    L = 520
+    rng = np.random.default_rng(21)
+    spans = [random_spans(L, rng, open_end=True), [(0, 100), (101, 102), (200, 519)],
+             [], [(5, 550)]]
+    meta, cache = build_cache(M, b, H, L_cap, d, dtype, L, spans, 31)
+    next_tok = torch.tensor([L, 300, L, 520], dtype=torch.int32, device=DEV)
+    before = bits(cache.kv)
+    tok0, pos0 = cache.tok_idx.cpu().numpy(), cache.pos_ids.cpu().numpy()
+    ref_out = torch.zeros_like(cache.kv)
+    # out of place first (kv untouched), then in place
+    kv_len0 = cache.kv_len.clone()
+    tok_save, pos_save = cache.tok_idx.clone(), cache.pos_ids.clone()
+    cache.compact(meta, next_tok, kv_out=ref_out)
+    assert np.array_equal(bits(cache.kv), before)
+    oop_len = cache.kv_len.clone()
+    cache.kv_len.copy_(kv_len0)
+    cache.tok_idx.copy_(tok_save)
+    cache.pos_ids.copy_(pos_save)
+    cache.compact(meta, next_tok)
+    torch.cuda.synchronize()
+    assert torch.equal(oop_len, cache.kv_len)
+    kvl = cache.kv_len.cpu().numpy()
+    after = bits(cache.kv)
+    oop = bits(ref_out)
+    ks = cache.kept_src.cpu().numpy()
+    tok, pos = cache.tok_idx.cpu().numpy(), cache.pos_ids.cpu().numpy()
+    for s in range(b):
+        types = O.token_types(spans[s], L_cap)
+        k_ = before[:, 0, s]
+        v_ = before[:, 1, s]
+        res = O.compact_cache(k_.reshape(-1, L_cap, d), v_.reshape(-1, L_cap, d), tok0[s], pos0[s],
+                              L, types, int(next_tok[s]))
+        n = res[4]
+        assert kvl[s] == n
+        assert np.array_equal(ks[s, :n], res[5]) and (ks[s, n:] == -1).all()
+        assert np.array_equal(tok[s, :n], res[2][:n])
+        assert np.array_equal(pos[s, :n], res[3][:n])
+        got_k = after[:, 0, s].reshape(-1, L_cap, d)[:, :n]
+        got_v = after[:, 1, s].reshape(-1, L_cap, d)[:, :n]
+        assert np.array_equal(got_k, res[0][:, :n]) and np.array_equal(got_v, res[1][:, :n])
+        assert np.array_equal(oop[:, :, s, :, :n], after[:, :, s, :, :n])
+    # idempotent
+    cache.compact(meta, next_tok)
+    torch.cuda.synchronize()
+    assert np.array_equal(cache.kv_len.cpu().numpy(), kvl)
+    assert np.array_equal(bits(cache.kv), after)
+
+
+def test_compaction_incremental_equals_one_shot():
+    say("compaction incremental")
+    M, b, H, L_cap, d = 1, 2, 2, 400, 64
+    L = 400
+    rng = np.random.default_rng(3)
+    spans = [random_spans(L, rng), random_spans(L, rng, start_at_zero=True)]
+    meta, one = build_cache(M, b, H, L_cap, d, "bf16", L, spans, 41)
+    _, inc = build_cache(M, b, H, L_cap, d, "bf16", L, spans, 41)
+    one.compact(meta, torch.full((b,), L, dtype=torch.int32, device=DEV))
+    for Pn in [50, 120, 121, 260, 399, 400]:
+        inc.compact(meta, torch.full((b,), Pn, dtype=torch.int32, device=DEV))
+    torch.cuda.synchronize()
+    assert torch.equal(one.kv_len, inc.kv_len)
+    n = int(one.kv_len.max())
+    for s in range(b):
+        ns = int(one.kv_len[s])
+        assert torch.equal(one.kv[:, :, s, :, :ns], inc.kv[:, :, s, :, :ns])
+        assert torch.equal(one.tok_idx[s, :ns], inc.tok_idx[s, :ns])
+    assert n > 0
+
+
+# ---------------------------------------------------------------------------
+# decode
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype,d,theta", [("bf16", 64, 0.0), ("bf16", 80, 10000.0),
+                                           ("f32", 64, 0.0), ("f32", 80, 10000.0)])
+def test_decode_matches_oracle(dtype, d, theta):
+    say(f"decode dtype={dtype} d={d} theta={theta}")
+    H, L_cap = 3, 700
+    lens = [0, 1, 255, 256, 257, 511, 600, 699]
+    b = len(lens)
+    spans = [[(650, 660)] for _ in range(b)]
+    meta = P().SpanMeta(spans, 1000, DEV)
+    cache = P().KVCache(1, b, H, L_cap, d, W().torch_dtype(dtype), DEV)
+    cache.kv.copy_(W().randn(cache.kv.shape, seed=51, dtype=dtype).to(DEV))
+    cache.kv_len.copy_(torch.tensor(lens, dtype=torch.int32))
+    toks = [700 + i for i in range(b)]
+    toks[2] = 650  # a <CL> step
+    cache.cur_tok.copy_(torch.tensor(toks, dtype=torch.int32))
+    ws = P().Workspace(b, H, 1, L_cap, d, DEV)
+    q, kn, vn = (rnd((b, H, d), 60 + i, dtype) for i in range(3))
+    o = torch.empty_like(q)
+    before = cache.kv.clone()
+    P().decode_layer(q, kn, vn, cache, 0, meta, ws, o, theta=theta)
+    torch.cuda.synchronize()
+    assert int(cache.status) == 0
+    assert torch.equal(cache.kv_len.cpu(), torch.tensor(lens, dtype=torch.int32))
+    Q, KN, VN, K, V, Og = f64(q), f64(kn), f64(vn), f64(before[0, 0]), f64(before[0, 1]), f64(o)
+    Kafter = f64(cache.kv[0, 0])
+    for s in range(b):
+        types = O.token_types(spans[s], 1000)
+        t = toks[s]
+        is_cl = types[t] == O.CL
+        qs, ks = Q[s], KN[s]
+        if theta > 0:
+            p = [O.tie_positions(types)[t]]
+            qs = np.stack([O.rope_rotate_half(Q[s, h][None], p, theta)[0] for h in range(H)])
+            ks = np.stack([O.rope_rotate_half(KN[s, h][None], p, theta)[0] for h in range(H)])
+        ref = O.decode_attention(qs, ks, VN[s], K[s], V[s], lens[s], is_cl)
+        if is_cl:
+            assert np.array_equal(Og[s], VN[s])
+            assert torch.equal(cache.kv[:, :, s], before[:, :, s])
+        else:
+            assert np.abs(Og[s] - ref).max() <= TOL[dtype], (s, np.abs(Og[s] - ref).max())
+            n = lens[s]
+            assert np.array_equal(f64(cache.kv[0, 1, s, :, n]), VN[s])
+            kerr = np.abs(Kafter[s, :, n] - ks)
+            assert kerr.max() <= (2e-2 if dtype == "bf16" else 1e-5)
+            assert torch.equal(cache.kv[:, :, s, :, :n], before[:, :, s, :, :n])
+
+
+def test_decode_reports_capacity_and_token_errors():
+    say("decode status")
+    H, L_cap, d = 2, 64, 64
+    meta = P().SpanMeta([[], []], 100, DEV)
+    cache = P().KVCache(1, 2, H, L_cap, d, torch.bfloat16, DEV)
+    cache.kv.zero_()
+    cache.kv_len.copy_(torch.tensor([L_cap, 3], dtype=torch.int32))
+    cache.cur_tok.copy_(torch.tensor([10, 100], dtype=torch.int32))
+    ws = P().Workspace(2, H, 1, L_cap, d, DEV)
+    q = rnd((2, H, d), 1, "bf16")
+    o = torch.zeros_like(q)
+    P().decode_layer(q, q, q, cache, 0, meta, ws, o)
+    torch.cuda.synchronize()
+    st = int(cache.status)
+    assert st & 1 and st & 2
+    assert torch.isnan(o.float()).all()
+    assert int(cache.kv.abs().sum()) == 0
+    cache.commit(meta)
+    torch.cuda.synchronize()
+    assert cache.kv_len.tolist() == [L_cap, 3]
+    assert cache.cur_tok.tolist() == [11, 101]
+
+
+# ---------------------------------------------------------------------------
+# the whole path on a small RoPE model: masked full cache == compacted cache
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype,d,theta", [("bf16", 80, 10000.0), ("f32", 64, 0.0)])
+def test_end_to_end_prompt_compact_decode(dtype, d, theta):
+    say(f"end to end dtype={dtype} d={d}")
+    M, b, H = 2, 2, 2
+    L, steps = 300, 100
+    T = L + steps
+    spans = [[(10, 50), (51, 52), (120, 250), (290, 330), (340, 341), (345, 380), (390, 420)],
+             [(0, 299), (305, 340), (360, 361)]]
+    types = [O.token_types(sp, T) for sp in spans]
+    cr_steps = sorted({r for sp in spans for _, r in sp if L <= r < T})
+    q, k, v = (rnd((M, b, H, T, d), 300 + i, dtype) for i in range(3))
+    meta = P().SpanMeta(spans, T, DEV)
+    cache = P().KVCache(M, b, H, T, d, W().torch_dtype(dtype), DEV)
+    ws = P().Workspace(b, H, L, T, d, DEV)
+    cache.start_prompt(L, meta)
+    outs_prompt = []
+    for m in range(M):
+        qr = torch.empty(b, H, L, d, dtype=q.dtype, device=DEV)
+        P().rope_rows(q[m, :, :, :L], qr, meta, L, 0, theta)
+        P().rope_rows(k[m, :, :, :L], cache.k(m), meta, L, 0, theta)
+        P().rope_rows(v[m, :, :, :L], cache.v(m), meta, L, 0, 0.0)
+        o = torch.empty_like(qr)
+        P().prefill_layer(qr, cache.k(m), cache.v(m), o, meta, ws, L)
+        outs_prompt.append(o)
+    cache.compact(meta)
+    step_out = torch.empty(steps, M, b, H, d, dtype=q.dtype, device=DEV)
+    for i, t in enumerate(range(L, T)):
+        for m in range(M):
+            qn = q[m, :, :, t].contiguous()
+            kn = k[m, :, :, t].contiguous()
+            vn = v[m, :, :, t].contiguous()
+            P().decode_layer(qn, kn, vn, cache, m, meta, ws, step_out[i, m], theta=theta)
+        cache.commit(meta)
+        if t in cr_steps:
+            cache.compact(meta)
+    torch.cuda.synchronize()
+    assert int(cache.status) == 0
+    Q, K, V = f64(q), f64(k), f64(v)
+    for m in range(M):
+        for s in range(b):
+            rp, rs, fin = O.run_prompt_and_decode(Q[m, s], K[m, s], V[m, s], types[s], L, steps,
+                                                  theta=theta, compact_after=cr_steps)
+            assert np.abs(f64(outs_prompt[m][s]) - rp).max() <= TOL[dtype]
+            got = f64(step_out[:, m, s])
+            assert np.abs(got - rs).max() <= TOL[dtype], np.abs(got - rs).max()
+            assert int(cache.kv_len[s]) == fin[4]
+            assert np.array_equal(cache.tok_idx[s, :fin[4]].cpu().numpy(), fin[2][:fin[4]])
+            assert np.array_equal(cache.pos_ids[s, :fin[4]].cpu().numpy(), fin[3][:fin[4]])
