@@ -1,0 +1,330 @@
+"""Benchmark of the sentinel-token compression hot path on one MI355X.
+
+One step = the whole path on one batch of the 3B-RoPE-shaped workload
+(32 layers, b=16, H=32, d_head=80, L=4096 transformed prompt tokens, half of
+them in <CL>..<CR> spans, rotary theta 10000):
+  * per layer: rotary embedding of Q and K at tied positions (K, and V, are
+    written into the layer's cache slice) and span-masked prefill attention;
+  * compaction of the whole (32, 2, 16, 32, 4096, 80) cache at the end of the
+    prompt (frees the closed spans' rows in place);
+  * 128 generated tokens: per token, 32 decode launches (one per layer: fused
+    rotary + append + split-K attention over the compacted cache) and one
+    commit.
+Inputs (prompt Q/K/V of every layer, the generated tokens' q/k/v) are
+synthetic N(0,1) bf16 tensors resident in HBM before timing starts.
+
+value = compacted-decode attention HBM throughput (algorithmic bytes of all
+decode launches / their summed HIP-event durations); the masked-prefill
+TFLOP/s is reported beside it.  Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, published
+PF_BQ, PF_BK = 128, 64         # prefill query block / gathered key tile
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="3b-rope")
+    ap.add_argument("--decode-steps", type=int, default=None)
+    ap.add_argument("--launch-events", choices=["all", "none"], default="all")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    return ap.parse_args()
+
+
+# ---------------------------------------------------------------------------
+# work accounting (host side, from the generated spans)
+# ---------------------------------------------------------------------------
+
+def last_visible_row(spans, L):
+    """Per column j: the last row that may attend to it (the mask's column
+    reach; <CL> columns reach only themselves)."""
+    vu = np.full(L, np.iinfo(np.int64).max, dtype=np.int64)
+    for c, r in spans:
+        if c < L:
+            vu[c] = c
+            vu[c + 1:min(r, L)] = r
+    return vu
+
+
+def prefill_work(spans_all, L, H, d):
+    """(algorithmic flops, executed flops) of one layer's prefill: 4*d per
+    visible (row, column) pair, and 4*d per pair of every 32x64 tile a wave
+    multiplies."""
+    alg = 0
+    exe = 0
+    for spans in spans_all:
+        vu = last_visible_row(spans, L)
+        cl = vu == np.arange(L)
+        # visible pairs: column j is seen by rows j..min(vu_j, L-1), CL only by itself
+        reach = np.minimum(vu, L - 1) - np.arange(L) + 1
+        nnz = int(reach.sum())
+        # CL rows see only themselves: remove what they would otherwise see
+        for i in np.nonzero(cl)[0]:
+            vis = int(((np.arange(i + 1) <= i) & (vu[:i + 1] >= i)).sum())
+            nnz -= vis - 1
+        alg += nnz
+        for I in range(0, L, PF_BQ):
+            jend = min(I + PF_BQ, L)
+            cols = np.nonzero(vu[:jend] >= I)[0]
+            nt = (len(cols) + PF_BK - 1) // PF_BK
+            for w in range(4):
+                Iw = I + 32 * w
+                if Iw >= L:
+                    continue
+                jmin = cols[::PF_BK][:nt]
+                exe += int((jmin <= Iw + 31).sum()) * PF_BK * 32
+    return 4 * d * alg * H, 4 * d * exe * H
+
+
+def kept_rows(spans, L):
+    """Rows left after freeing every span closed before index L (closed form:
+    L minus the closed spans' lengths minus the <CL> of a span still open)."""
+    closed = sum(r - c for c, r in spans if r < L)
+    open_cl = sum(1 for c, r in spans if c < L <= r)
+    return L - closed - open_cl
+
+
+# ---------------------------------------------------------------------------
+# CPU baseline: the oracle on a bounded sample
+# ---------------------------------------------------------------------------
+
+def cpu_baseline(w, spans_all, k_in, v_in, q_dec, k_dec, v_dec, seconds):
+    """The oracle's decode (rotary + attention over its own compacted cache)
+    on whole (layer, sequence) samples until about `seconds` of CPU time."""
+    from oracle import sckv_oracle as O
+    cores = len(os.sched_getaffinity(0))
+    L, H, d, M, b = w.seq_len, w.heads, w.d_head, w.layers, w.batch
+    T = L + w.decode_steps
+    f = lambda t: t.detach().to("cpu").double().numpy()
+    bytes_done, t_dec, samples, steps_done = 0, 0.0, 0, 0
+    for i in range(M * b):
+        if t_dec >= seconds:
+            break
+        m, s = i % M, (i * 7) % b
+        types = O.token_types(spans_all[s], T)
+        pos = O.tie_positions(types)
+        K = np.stack([O.rope_rotate_half(f(k_in[m, s, h]), pos[:L], w.rope_theta) for h in range(H)])
+        Kc = np.zeros((H, T, d)); Vc = np.zeros((H, T, d))
+        Kc[:, :L], Vc[:, :L] = K, f(v_in[m, s])
+        tok = np.zeros(T, np.int64); tok[:L] = np.arange(L)
+        pp = np.zeros(T, np.int64); pp[:L] = pos[:L]
+        Kc, Vc, tok, pp, n, _ = O.compact_cache(Kc, Vc, tok, pp, L, types, L)
+        qd, kd, vd = f(q_dec[:, m, s]), f(k_dec[:, m, s]), f(v_dec[:, m, s])
+        for st in range(w.decode_steps):
+            t = L + st
+            t0 = time.perf_counter()
+            qr = np.stack([O.rope_rotate_half(qd[st, h][None], [pos[t]], w.rope_theta)[0] for h in range(H)])
+            kr = np.stack([O.rope_rotate_half(kd[st, h][None], [pos[t]], w.rope_theta)[0] for h in range(H)])
+            O.decode_attention(qr, kr, vd[st], Kc, Vc, n, types[t] == O.CL)
+            t_dec += time.perf_counter() - t0
+            Kc[:, n], Vc[:, n] = kr, vd[st]
+            n += 1
+            bytes_done += n * H * d * 2 * 2 + 6 * H * d * 2
+            steps_done += 1
+        samples += 1
+    return {"value": round(bytes_done / t_dec / 1e9, 4), "unit": "GB/s", "cores": cores,
+            "kind": "oracle",
+            "sample": f"fp64 NumPy oracle decode (rotary + attention over its own compacted "
+                      f"cache), {samples} whole (layer, sequence) slices x {H} heads x "
+                      f"{w.decode_steps} generated tokens = {steps_done} sequence-steps, "
+                      f"{t_dec:.1f} s of CPU time; bytes counted as for the GPU figure"}
+
+
+# ---------------------------------------------------------------------------
+# main
+# ---------------------------------------------------------------------------
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on exactly one GPU: the sentinel-token compression path shards "
+              "over sequences/heads/layers with no exchange, so multi-GPU figures are not "
+              "produced by this build (pass --gpus 1).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2310_08152_amd import path as P
+    from paper_2310_08152_amd import workload as W
+
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    w = W.get_workload(args.workload)
+    steps = w.decode_steps if args.decode_steps is None else args.decode_steps
+    M, b, H, d, L = w.layers, w.batch, w.heads, w.d_head, w.seq_len
+    theta = w.rope_theta
+    T = L + steps
+    spans_all = W.workload_spans(w)
+    L_cap = max(L, max(kept_rows(s, L) for s in spans_all) + steps)
+
+    # ---- inputs resident in HBM ----
+    dt = W.torch_dtype(w.dtype)
+    q_in = torch.empty(M, b, H, L, d, dtype=dt, device=dev)
+    k_in = torch.empty_like(q_in)
+    v_in = torch.empty_like(q_in)
+    for m in range(M):
+        for i, t in enumerate((q_in, k_in, v_in)):
+            t[m].copy_(W.randn((b, H, L, d), seed=w.seed * 100000 + m * 10 + i, dtype=w.dtype,
+                               device=dev))
+    q_dec = W.randn((steps, M, b, H, d), seed=w.seed * 100000 + 7001, dtype=w.dtype, device=dev)
+    k_dec = W.randn((steps, M, b, H, d), seed=w.seed * 100000 + 7002, dtype=w.dtype, device=dev)
+    v_dec = W.randn((steps, M, b, H, d), seed=w.seed * 100000 + 7003, dtype=w.dtype, device=dev)
+
+    meta = P.SpanMeta(spans_all, T, dev)
+    cache = P.KVCache(M, b, H, L_cap, d, dt, dev)
+    ws = P.Workspace(b, H, L, L_cap, d, dev)
+    qr = torch.empty(b, H, L, d, dtype=dt, device=dev)
+    o = torch.empty(b, H, L, d, dtype=dt, device=dev)
+    od = torch.empty(b, H, d, dtype=dt, device=dev)
+    torch.cuda.synchronize()
+
+    n_dec = steps * M
+    use_ev = args.launch_events == "all"
+    E = lambda: torch.cuda.Event(enable_timing=True)
+
+    def run_step(rec):
+        if rec is not None:
+            rec["t0"].record()
+        cache.start_prompt(L, meta)
+        for m in range(M):
+            P.rope_rows(q_in[m], qr, meta, L, 0, theta)
+            P.rope_rows(k_in[m], cache.k(m), meta, L, 0, theta)
+            P.rope_rows(v_in[m], cache.v(m), meta, L, 0, 0.0)
+            if rec is not None and use_ev:
+                rec["pf"][m][0].record()
+            P.prefill_layer(qr, cache.k(m), cache.v(m), o, meta, ws, L)
+            if rec is not None and use_ev:
+                rec["pf"][m][1].record()
+        if rec is not None:
+            rec["t1"].record()
+        cache.compact(meta)
+        if rec is not None:
+            rec["t2"].record()
+        for t in range(steps):
+            for m in range(M):
+                if rec is not None and use_ev:
+                    rec["dec"][t * M + m][0].record()
+                P.decode_layer(q_dec[t, m], k_dec[t, m], v_dec[t, m], cache, m, meta, ws, od,
+                               theta=theta)
+                if rec is not None and use_ev:
+                    rec["dec"][t * M + m][1].record()
+            cache.commit(meta)
+        if rec is not None:
+            rec["t3"].record()
+
+    for _ in range(args.warmup):
+        run_step(None)
+    torch.cuda.synchronize()
+    recs = []
+    for _ in range(args.steps):
+        recs.append({"t0": E(), "t1": E(), "t2": E(), "t3": E(),
+                     "pf": [(E(), E()) for _ in range(M)] if use_ev else None,
+                     "dec": [(E(), E()) for _ in range(n_dec)] if use_ev else None})
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    for r in recs:
+        run_step(r)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    status = int(cache.status)
+    if status:
+        raise RuntimeError(f"device status {status}")
+
+    # ---- accounting ----
+    n_keep = np.array([kept_rows(s, L) for s in spans_all], dtype=np.int64)
+    assert np.array_equal(cache.kv_len.cpu().numpy(), n_keep + steps), "unexpected kv_len"
+    row_bytes = d * 2 * 2                    # one K row + one V row (bf16)
+    io_bytes = 6 * b * H * d * 2             # q, k_new, v_new read; o, new K/V row written
+    dec_bytes = [int((n_keep + t + 1).sum()) * H * row_bytes + io_bytes for t in range(steps)]
+    dec_bytes_step = M * sum(dec_bytes)
+    pf_alg, pf_exe = prefill_work(spans_all, L, H, d)
+    comp_bytes = 0
+    for spans in spans_all:
+        vu = last_visible_row(spans, L)
+        keep = (vu != np.arange(L)) & (vu >= L)
+        rank = np.cumsum(keep) - 1
+        comp_bytes += int((keep & (rank != np.arange(L))).sum())
+    comp_bytes *= 2 * M * H * d * 2 * 2      # read + write of every moved row, K and V
+
+    step_ms = [r["t0"].elapsed_time(r["t3"]) for r in recs]
+    pre_ms = [r["t0"].elapsed_time(r["t1"]) for r in recs]
+    cmp_ms = [r["t1"].elapsed_time(r["t2"]) for r in recs]
+    decph_ms = [r["t2"].elapsed_time(r["t3"]) for r in recs]
+    if use_ev:
+        dec_launch_ms = np.array([[a.elapsed_time(z) for a, z in r["dec"]] for r in recs])
+        pf_launch_ms = np.array([[a.elapsed_time(z) for a, z in r["pf"]] for r in recs])
+        dec_avg_ms = float(dec_launch_ms.mean())
+        pf_avg_ms = float(pf_launch_ms.mean())
+        dec_total_ms = float(dec_launch_ms.sum(axis=1).mean())
+    else:
+        dec_avg_ms = float(np.mean(decph_ms)) / n_dec
+        pf_avg_ms = float(np.mean(pre_ms)) / M
+        dec_total_ms = float(np.mean(decph_ms))
+    dec_gbs = dec_bytes_step / (dec_total_ms * 1e-3) / 1e9
+    dec_bytes_launch = dec_bytes_step / n_dec
+    pf_tflops_exe = pf_exe / (pf_avg_ms * 1e-3) / 1e12
+    pf_tflops_alg = pf_alg / (pf_avg_ms * 1e-3) / 1e12
+    ms_per_step = float(np.mean(step_ms))
+
+    out = {
+        "metric": "compacted-decode attn HBM GB/s + masked-prefill TFLOP/s vs MI355X roofline",
+        "value": round(dec_gbs, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}: prefill+compaction+decode", "layers": M, "batch": b,
+                   "heads": H, "d_head": d, "seq_len": L, "evicted": 0.5,
+                   "decode_steps": steps, "rope_theta": theta, "L_cap": L_cap,
+                   "parallelism": "single-gpu"},
+        "roofline": {"bound": "hbm", "kernel": "decode_chunk_kernel (compacted_decode_attn)",
+                     "achieved": round(dec_bytes_launch / (dec_avg_ms * 1e-3) / 1e9, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(dec_bytes_launch / (dec_avg_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                     "traffic": None, "avg_launch_us": round(dec_avg_ms * 1e3, 2),
+                     "bytes_per_launch": int(dec_bytes_launch)},
+        "roofline_prefill": {"bound": "mfma", "kernel": "prefill_attn_kernel (span_masked_prefill_attn)",
+                             "achieved": round(pf_tflops_exe, 1), "peak": BF16_PEAK_TFLOPS,
+                             "unit": "TFLOP/s", "frac": round(pf_tflops_exe / BF16_PEAK_TFLOPS, 4),
+                             "algorithmic_tflops": round(pf_tflops_alg, 1),
+                             "executed_over_algorithmic": round(pf_exe / pf_alg, 3),
+                             "avg_launch_us": round(pf_avg_ms * 1e3, 1)},
+        "phases_ms": {"rope+prefill": round(float(np.mean(pre_ms)), 3),
+                      "compaction": round(float(np.mean(cmp_ms)), 3),
+                      "decode": round(float(np.mean(decph_ms)), 3)},
+        "compaction_gbs": round(comp_bytes / (float(np.mean(cmp_ms)) * 1e-3) / 1e9, 1),
+        "wall_s_timed": round(wall, 3),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, spans_all, k_in, v_in, q_dec, k_dec, v_dec,
+                                           args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

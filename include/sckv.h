@@ -188,8 +188,12 @@ int kv_compact(void* kv, void* kv_out, int32_t M, int32_t b, int32_t H, int32_t 
  * q, k_new, v_new, o : (b, H, d_head) contiguous.
  * k_cache, v_cache   : (b, H, L_cap, d_head) layer slices (kv[m,0], kv[m,1]).
  * kv_len, cur_tok    : [b].   vu, pos: [b][L_meta].
- * ws     : device workspace >= sckv_decode_workspace_bytes(b, H, L_cap, d_head).
+ * ws     : device workspace >= sckv_decode_workspace_bytes(b, H, L_cap, d_head)
+ *          holding the split-K partials (overwritten; calls that share a
+ *          workspace must be ordered, e.g. enqueued on one stream).
  * status : nullable int32, status bits OR-ed in.
+ * The key rows are split into chunks of 256 rows, one workgroup each; a
+ * second kernel merges the chunk partials (log-sum-exp) into o.
  * ------------------------------------------------------------------------- */
 size_t sckv_decode_workspace_bytes(int32_t b, int32_t H, int32_t L_cap, int32_t d_head);
 int compacted_decode_attn(const void* q, const void* k_new, const void* v_new, void* k_cache,

@@ -2,14 +2,19 @@
 // Section 1 and Section 2 (the key/value memory read per step drives decode
 // cost) and Section 4.3 (generation continues from the compressed cache).
 //
-// decode_chunk_kernel : grid (chunks, b*H).  Each workgroup streams CH rows of
-//   one (sequence, head) slice: a 16-byte piece per lane, a row spread over
-//   LPR lanes (a power-of-two group of GRP lanes, so the row dot product is a
-//   butterfly inside the group), an online softmax per lane group, then the
-//   groups of the workgroup are merged through LDS into one partial
-//   (max, sum, unnormalised output) in log2 units.  The workgroup whose chunk
-//   holds row kv_len also rotates and writes the new key/value pair there.
-// decode_combine_kernel : merges the partials of each slice (log-sum-exp).
+// decode_chunk_kernel : one workgroup per (sequence, head, chunk of CH rows),
+//   in an XCD-aware order so that the chunks of one slice share an L2.  A
+//   workgroup streams its rows with a 16-byte piece per lane; a row is spread
+//   over LPR lanes of an aligned power-of-two group of GRP lanes, so the row
+//   dot product is a DPP butterfly inside the group.  Each lane group keeps an
+//   online softmax; the groups of the workgroup are merged through LDS into
+//   one partial (max, sum, unnormalised output) in log2 units.  The
+//   workgroup whose chunk holds row kv_len also rotates the new key and writes
+//   the new key/value pair there.
+// decode_combine_kernel : merges the partials of each slice (log-sum-exp) and
+//   writes the output; a <CL> step outputs v_new, a failed step NaN.  Being a
+//   separate launch on the same stream, it sees every partial without any
+//   device-wide cache flush inside the chunk kernel.
 #include <math.h>
 
 #include <cmath>
@@ -23,7 +28,7 @@ constexpr int DEC_CH = 256;  // rows per chunk
 constexpr float LOG2E = 1.4426950408889634f;
 
 struct RopeTab {
-  double w[40];
+  double w[40];  // theta^(-2i/d), i < d/2
 };
 
 template <typename T, int D>
@@ -36,13 +41,13 @@ struct DecCfg {
   static constexpr int NG = (DEC_THREADS / 64) * RPW;  // lane groups per workgroup
 };
 
-// rotated piece `seg` of a head vector x (global), rotate-half convention
+// rotated piece `seg` of a head vector x (global), rotate-half convention;
+// inv[i] = theta^(-2i/d) (LDS)
 template <typename T, int D>
 __device__ __forceinline__ void load_rotated_piece(const T* x, int seg, bool rotate, double ps,
-                                                   const RopeTab& tab, float* out) {
+                                                   const double* inv, float* out) {
   constexpr int E = Piece<T>::E;
   constexpr int LPR = D / E;
-  constexpr int HALF = D / 2;
   Piece<T>::unpack(ld16(x + seg * E), out);
   if (!rotate) return;
   const bool first = seg < LPR / 2;
@@ -50,10 +55,10 @@ __device__ __forceinline__ void load_rotated_piece(const T* x, int seg, bool rot
   float partner[E];
   Piece<T>::unpack(ld16(x + pseg * E), partner);
   const double two_pi = 6.283185307179586476925286766559;
+  const int i0 = (first ? seg : pseg) * E;
 #pragma unroll
   for (int e = 0; e < E; ++e) {
-    const int i = (seg * E + e) % HALF;
-    double ang = ps * tab.w[i];
+    double ang = ps * inv[i0 + e];
     ang -= two_pi * rint(ang / two_pi);
     float sn, cs;
     sincosf((float)ang, &sn, &cs);
@@ -61,21 +66,15 @@ __device__ __forceinline__ void load_rotated_piece(const T* x, int seg, bool rot
   }
 }
 
-template <int GRP>
-__device__ __forceinline__ float group_sum(float x) {
-#pragma unroll
-  for (int o = 1; o < GRP; o <<= 1) x += __shfl_xor(x, o, 64);
-  return x;
-}
-
-// Returns true (and reports) if the sequence's step is not an ordinary append.
+// 0: ordinary append step; 1: <CL> step; 2: token outside [0, L_meta);
+// 3: no room for the new row
 __device__ __forceinline__ int step_kind(const int32_t* cur_tok, const int32_t* vu,
                                          const int32_t* kv_len, int s, int L_meta, int L_cap) {
   const int t = cur_tok[s];
-  if (t < 0 || t >= L_meta) return 2;                 // bad token
-  if (vu[(int64_t)s * L_meta + t] == t) return 1;      // <CL>
+  if (t < 0 || t >= L_meta) return 2;
+  if (vu[(int64_t)s * L_meta + t] == t) return 1;
   const int n = kv_len[s];
-  if (n < 0 || n >= L_cap) return 3;                   // no room
+  if (n < 0 || n >= L_cap) return 3;
   return 0;
 }
 
@@ -85,19 +84,17 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_chunk_kernel(
     T* __restrict__ k_cache, T* __restrict__ v_cache, const int32_t* __restrict__ kv_len,
     const int32_t* __restrict__ cur_tok, const int32_t* __restrict__ vu,
     const int32_t* __restrict__ pos, int32_t L_meta, int32_t H, int32_t L_cap, float qscale,
-    int rotate, RopeTab tab, float* __restrict__ part, int32_t n_chunk_max,
-    int32_t* __restrict__ status) {
+    int rotate, RopeTab tab, float* __restrict__ part, int32_t n_chunk_max, int32_t n_work) {
   using C = DecCfg<T, D>;
   constexpr int E = C::E, LPR = C::LPR, GRP = C::GRP, RPW = C::RPW, U = C::U, NG = C::NG;
-  const int bh = blockIdx.y;
+  const int x = blockIdx.x;
+  const int xcd = x & 7, idx = x >> 3;
+  const int qn = n_work >> 3, rem = n_work & 7;
+  const int work = xcd * qn + min(xcd, rem) + idx;
+  const int bh = work / n_chunk_max;
+  const int chunk = work % n_chunk_max;
   const int s = bh / H;
-  const int chunk = blockIdx.x;
-  const int kind = step_kind(cur_tok, vu, kv_len, s, L_meta, L_cap);
-  if (kind != 0) {
-    if (kind >= 2 && chunk == 0 && threadIdx.x == 0 && (bh % H) == 0 && status)
-      atomicOr(status, kind == 2 ? SCKV_STATUS_TOKEN : SCKV_STATUS_CAP);
-    return;
-  }
+  if (step_kind(cur_tok, vu, kv_len, s, L_meta, L_cap) != 0) return;  // combine handles it
   const int n = kv_len[s];
   const int rows = n + 1;
   const int r0 = chunk * DEC_CH;
@@ -112,12 +109,16 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_chunk_kernel(
   const int seg = lane % GRP;    // piece within the row
   const bool active = seg < LPR;
 
+  __shared__ double inv[D / 2];
+  if (rotate && tid < D / 2) inv[tid] = tab.w[tid];
+  __syncthreads();
+
   const double ps = rotate ? (double)pos[(int64_t)s * L_meta + cur_tok[s]] : 0.0;
   float qf[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) qf[e] = 0.f;
   if (active) {
-    load_rotated_piece<T, D>(q + (int64_t)bh * D, seg, rotate, ps, tab, qf);
+    load_rotated_piece<T, D>(q + (int64_t)bh * D, seg, rotate, ps, inv, qf);
 #pragma unroll
     for (int e = 0; e < E; ++e) qf[e] *= qscale;  // scores come out in log2 units
   }
@@ -182,7 +183,7 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_chunk_kernel(
 #pragma unroll
     for (int e = 0; e < E; ++e) { kf[e] = 0.f; vf[e] = 0.f; }
     if (active) {
-      load_rotated_piece<T, D>(k_new + (int64_t)bh * D, seg, rotate, ps, tab, kf);
+      load_rotated_piece<T, D>(k_new + (int64_t)bh * D, seg, rotate, ps, inv, kf);
       // score with the stored (rounded) key, exactly as later steps will see it
       Piece<T>::unpack(Piece<T>::pack(kf), kf);
       Piece<T>::unpack(ld16(v_new + (int64_t)bh * D + seg * E), vf);
@@ -205,7 +206,7 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_chunk_kernel(
     }
   }
 
-  // merge the lane groups of the workgroup
+  // merge the lane groups of the workgroup into this chunk's partial
   __shared__ float sm[NG], sl[NG];
   __shared__ float sacc[NG][D];
   const int grp = wave * RPW + g;
@@ -219,14 +220,14 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_chunk_kernel(
   if (tid < D) {
     float M = -INFINITY;
     for (int i = 0; i < NG; ++i) M = fmaxf(M, sm[i]);
-    float Lsum = 0.f, o = 0.f;
+    float Lsum = 0.f, ov = 0.f;
     for (int i = 0; i < NG; ++i) {
       if (sm[i] == -INFINITY) continue;
       const float w = exp2f(sm[i] - M);
       Lsum += sl[i] * w;
-      o += sacc[i][tid] * w;
+      ov += sacc[i][tid] * w;
     }
-    out[2 + tid] = o;
+    out[2 + tid] = ov;
     if (tid == 0) { out[0] = M; out[1] = Lsum; }
   }
 }
@@ -236,12 +237,14 @@ __global__ __launch_bounds__(128) void decode_combine_kernel(
     const T* __restrict__ v_new, const int32_t* __restrict__ kv_len,
     const int32_t* __restrict__ cur_tok, const int32_t* __restrict__ vu, int32_t L_meta,
     int32_t H, int32_t L_cap, const float* __restrict__ part, int32_t n_chunk_max,
-    T* __restrict__ o) {
+    T* __restrict__ o, int32_t* __restrict__ status) {
   constexpr int E = Piece<T>::E;
   const int bh = blockIdx.x;
   const int s = bh / H;
   const int tid = threadIdx.x;
   const int kind = step_kind(cur_tok, vu, kv_len, s, L_meta, L_cap);
+  if (kind >= 2 && tid == 0 && (bh % H) == 0 && status)
+    atomicOr(status, kind == 2 ? SCKV_STATUS_TOKEN : SCKV_STATUS_CAP);
   __shared__ float res[D];
   if (tid < D) {
     float r;
@@ -292,16 +295,16 @@ static int launch_decode(const void* q, const void* k_new, const void* v_new, vo
     for (int i = 0; i < D / 2; ++i) tab.w[i] = std::pow((double)theta, -2.0 * i / D);
   const int nc = n_chunks(L_cap);
   float* part = static_cast<float*>(ws);
-  dim3 grid(nc, b * H);
-  decode_chunk_kernel<T, D><<<grid, DEC_THREADS, 0, stream>>>(
+  const int n_work = b * H * nc;
+  decode_chunk_kernel<T, D><<<n_work, DEC_THREADS, 0, stream>>>(
       static_cast<const T*>(q), static_cast<const T*>(k_new), static_cast<const T*>(v_new),
       static_cast<T*>(k_cache), static_cast<T*>(v_cache), kv_len, cur_tok, vu, pos, L_meta, H,
-      L_cap, scale * LOG2E, rotate, tab, part, nc, status);
+      L_cap, scale * LOG2E, rotate, tab, part, nc, n_work);
   int rc = hip_check(hipGetLastError(), "compacted_decode_attn: chunk launch");
   if (rc) return rc;
   decode_combine_kernel<T, D><<<b * H, 128, 0, stream>>>(
       static_cast<const T*>(v_new), kv_len, cur_tok, vu, L_meta, H, L_cap, part, nc,
-      static_cast<T*>(o));
+      static_cast<T*>(o), status);
   return hip_check(hipGetLastError(), "compacted_decode_attn: combine launch");
 }
 
@@ -328,9 +331,8 @@ extern "C" int compacted_decode_attn(const void* q, const void* k_new, const voi
   if (!supported_d(d_head)) return fail(SCKV_EUNSUP, "compacted_decode_attn: d_head must be 64 or 80");
   if (b <= 0 || H <= 0 || L_cap <= 0 || L_meta <= 0)
     return fail(SCKV_EINVAL, "compacted_decode_attn: sizes must be positive");
-  if ((int64_t)b * H > 0x7fffffff / 2 || (int64_t)b * H > 65535 * 32768)
-    return fail(SCKV_EUNSUP, "compacted_decode_attn: b*H too large");
-  if ((int64_t)b * H > 65535) return fail(SCKV_EUNSUP, "compacted_decode_attn: b*H above 65535");
+  if ((int64_t)b * H * n_chunks(L_cap) > 0x7fffffff)
+    return fail(SCKV_EUNSUP, "compacted_decode_attn: b*H*chunks too large");
   if (!(scale > 0.f) || std::isinf(scale)) return fail(SCKV_EINVAL, "compacted_decode_attn: scale must be finite and > 0");
   if (!(rope_theta >= 0.f) || std::isinf(rope_theta))
     return fail(SCKV_EINVAL, "compacted_decode_attn: rope_theta must be finite and >= 0");

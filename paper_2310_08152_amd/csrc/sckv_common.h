@@ -81,6 +81,29 @@ __device__ __forceinline__ void st16(void* p, const u32x4& v) { *reinterpret_cas
 // wait until every outstanding vector-memory load of this wave has returned
 __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
+// cross-lane moves inside a row of 16 lanes (DPP; no LDS traffic)
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL,
+                                                               0xf, 0xf, false));
+}
+constexpr int DPP_QUAD_XOR1 = 0xb1;      // quad_perm [1,0,3,2]
+constexpr int DPP_QUAD_XOR2 = 0x4e;      // quad_perm [2,3,0,1]
+constexpr int DPP_ROW_MIRROR = 0x140;    // lane i <- lane 15-i within a row
+constexpr int DPP_ROW_HALF_MIRROR = 0x141;  // lane i <- lane 7-i within a half row
+
+// sum over aligned groups of GRP lanes (8, 16 or 32); every lane gets the sum
+template <int GRP>
+__device__ __forceinline__ float group_sum(float x) {
+  static_assert(GRP == 8 || GRP == 16 || GRP == 32, "group size");
+  x += dpp_mov<DPP_QUAD_XOR1>(x);
+  x += dpp_mov<DPP_QUAD_XOR2>(x);
+  x += dpp_mov<DPP_ROW_HALF_MIRROR>(x);
+  if constexpr (GRP >= 16) x += dpp_mov<DPP_ROW_MIRROR>(x);
+  if constexpr (GRP >= 32) x += __shfl_xor(x, 16, 64);
+  return x;
+}
+
 __device__ __forceinline__ int lane_id() { return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0)); }
 
 // number of set bits of a 64-bit wave mask strictly below this lane
