@@ -47,6 +47,8 @@ def parse():
     ap.add_argument("--launch-events", choices=["all", "none"], default="all")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--gen-tokens", type=int, default=None,
+                    help="streaming workload: generated tokens per run (default: all)")
     return ap.parse_args()
 
 
@@ -149,6 +151,112 @@ def cpu_baseline(w, spans_all, k_in, v_in, q_dec, k_dec, v_dec, seconds):
                       f"{t_dec:.1f} s of CPU time; bytes counted as for the GPU figure"}
 
 
+
+# ---------------------------------------------------------------------------
+# streaming workload: spans open and close in the generated text
+# ---------------------------------------------------------------------------
+
+def live_rows_schedule(spans, prompt, gen):
+    """Rows held after each generated token when every closed span is freed
+    right after its <CR> (host bookkeeping from the span list), and the peak
+    row count, reached just before a span is freed."""
+    out = []
+    n = prompt
+    peak = prompt
+    closes = {r: (r - c) for c, r in spans}
+    cls = {c for c, _ in spans}
+    for t in range(prompt, prompt + gen):
+        if t not in cls:
+            n += 1
+        peak = max(peak, n)
+        if t in closes:
+            n -= closes[t] - 1  # the <CL> was never appended
+        out.append(n)
+    return out, peak
+
+
+def run_streaming(args, w):
+    import torch
+
+    from paper_2310_08152_amd import path as P
+    from paper_2310_08152_amd import workload as W
+
+    dev = "cuda:0"
+    gen = w.gen_tokens if args.gen_tokens is None else args.gen_tokens
+    M, b, H, d, L = w.layers, w.batch, w.heads, w.d_head, w.seq_len
+    T = L + gen
+    dt = W.torch_dtype(w.dtype)
+    POOL = 16  # distinct synthetic token inputs, used cyclically
+    qp = W.randn((POOL, M, b, H, d), seed=w.seed * 100000 + 1, dtype=w.dtype, device=dev)
+    kp = W.randn((POOL, M, b, H, d), seed=w.seed * 100000 + 2, dtype=w.dtype, device=dev)
+    vp = W.randn((POOL, M, b, H, d), seed=w.seed * 100000 + 3, dtype=w.dtype, device=dev)
+    od = torch.empty(b, H, d, dtype=dt, device=dev)
+    results = {}
+    for mode in ("compressed", "uncompressed"):
+        spans = [[(c, r) for c, r in s if c < T] for s in W.workload_spans(w)] \
+            if mode == "compressed" else [[] for _ in range(b)]
+        sched, peak = live_rows_schedule(spans[0], L, gen)
+        L_cap = peak
+        cr_steps = {r for c, r in spans[0] if L <= r < T}
+        meta = P.SpanMeta(spans, T, dev)
+        cache = P.KVCache(M, b, H, L_cap, d, dt, dev)
+        for m in range(M):
+            for kv in range(2):
+                cache.kv[m, kv, :, :, :L].copy_(W.randn((b, H, L, d), seed=w.seed * 1000 + m * 2 + kv,
+                                                        dtype=w.dtype, device=dev))
+        ws = P.Workspace(b, H, 1, L_cap, d, dev)
+
+        def loop():
+            cache.start_prompt(L, meta)
+            for t in range(gen):
+                i = t % POOL
+                for m in range(M):
+                    P.decode_layer(qp[i, m], kp[i, m], vp[i, m], cache, m, meta, ws, od,
+                                   theta=w.rope_theta)
+                cache.commit(meta)
+                if L + t in cr_steps:
+                    cache.compact(meta)
+
+        if args.warmup:
+            loop()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        loop()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        if int(cache.status):
+            raise RuntimeError(f"device status {int(cache.status)}")
+        assert cache.kv_len.tolist() == [sched[-1]] * b, (cache.kv_len.tolist()[:4], sched[-1])
+        row_b = d * 2
+        rows_read = sum(sched[t] for t in range(gen))  # rows attended per (seq, head, layer)
+        results[mode] = {
+            "tokens_per_s": round(b * gen / (ms * 1e-3), 1),
+            "ms": round(ms, 2),
+            "peak_rows": peak, "final_rows": sched[-1],
+            "cache_bytes": int(cache.kv.numel() * cache.kv.element_size()),
+            "attn_gbs": round(rows_read * b * H * M * row_b * 2 / (ms * 1e-3) / 1e9, 1),
+        }
+        del cache, meta, ws
+        torch.cuda.empty_cache()
+    c, u = results["compressed"], results["uncompressed"]
+    out = {
+        "metric": "streaming attention tokens/s and peak KV bytes, compressed vs uncompressed cache",
+        "value": c["tokens_per_s"], "unit": "tokens/s", "n_gpus": 1, "steps": 1,
+        "warmup": args.warmup, "ms_per_step": c["ms"], "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": f"{w.name}: decode {gen} tokens after a {L}-token prompt, "
+                               f"in-place compaction after every <CR>", "layers": M, "batch": b,
+                   "heads": H, "d_head": d, "prompt": L, "generated": gen,
+                   "parallelism": "single-gpu"},
+        "compressed": c, "uncompressed": u,
+        "speedup_vs_uncompressed": round(c["tokens_per_s"] / u["tokens_per_s"], 3),
+        "kv_bytes_saved": u["cache_bytes"] - c["cache_bytes"],
+    }
+    print(json.dumps(out), flush=True)
+
+
 # ---------------------------------------------------------------------------
 # main
 # ---------------------------------------------------------------------------
@@ -169,6 +277,8 @@ def main():
     dev = "cuda:0"
     torch.cuda.set_device(0)
     w = W.get_workload(args.workload)
+    if w.gen_tokens > 0:
+        return run_streaming(args, w)
     steps = w.decode_steps if args.decode_steps is None else args.decode_steps
     M, b, H, d, L = w.layers, w.batch, w.heads, w.d_head, w.seq_len
     theta = w.rope_theta

@@ -1,0 +1,191 @@
+"""Full-size parity in the launch configuration the benchmark times, checked
+on sampled outputs the oracle can compute one slice at a time.  Indices,
+lengths and positions are checked for every sequence, bit for bit."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import sckv_oracle as O
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+TOL = 2e-2
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def P():
+    from paper_2310_08152_amd import path
+    return path
+
+
+def W():
+    from paper_2310_08152_amd import workload
+    return workload
+
+
+def f64(t):
+    return t.detach().to("cpu", torch.float64).numpy()
+
+
+def say(msg):
+    print(msg, flush=True)
+
+
+def oracle_slice(K0, V0, L, types, pos, qd, kd, vd, theta, cr_steps, check):
+    """The oracle's view of one (layer, sequence, head) slice: cache rows
+    [0, L) as stored before compaction, freed at L, then one decode step per
+    row of qd/kd/vd (raw, unrotated), compacted again after every <CR>.
+    Returns {step (1-based): output}."""
+    d = K0.shape[-1]
+    steps = len(qd)
+    T = L + steps
+    Kc = np.zeros((1, T, d)); Vc = np.zeros((1, T, d))
+    Kc[0, :L], Vc[0, :L] = K0, V0
+    tok = np.zeros(T, np.int64); tok[:L] = np.arange(L)
+    pp = np.zeros(T, np.int64); pp[:L] = pos[:L]
+    Kc, Vc, tok, pp, n, _ = O.compact_cache(Kc, Vc, tok, pp, L, types, L)
+    out = {}
+    for i in range(steps):
+        t = L + i
+        qr, kr = qd[i][None], kd[i][None]
+        if theta > 0:
+            qr = O.rope_rotate_half(qr, [pos[t]], theta)
+            kr = O.rope_rotate_half(kr, [pos[t]], theta)
+        is_cl = types[t] == O.CL
+        o = O.decode_attention(qr, kr, vd[i][None], Kc, Vc, n, is_cl)
+        if i + 1 in check:
+            out[i + 1] = o[0]
+        if not is_cl:
+            Kc[0, n], Vc[0, n] = kr[0], vd[i]
+            tok[n], pp[n] = t, pos[t]
+            n += 1
+        if t in cr_steps:
+            Kc, Vc, tok, pp, n, _ = O.compact_cache(Kc, Vc, tok, pp, n, types, t + 1)
+    return out
+
+
+def run_decode_workload(w, steps, samples, check, prefill_layer=None, prefill_heads=()):
+    """Fill the cache with the prompt (rotary keys for the prefill layer),
+    optionally run prefill on one layer, compact at the end of the prompt,
+    run `steps` decode steps over all layers, and check samples."""
+    M, b, H, d, L = w.layers, w.batch, w.heads, w.d_head, w.seq_len
+    theta = w.rope_theta
+    T = L + steps
+    spans = [[(c, r) for c, r in s if c < T] for s in W().workload_spans(w)]
+    types = [O.token_types(s, T) for s in spans]
+    pos = [O.tie_positions(t) for t in types]
+    keep_n = [int(O.keep_rows(t, L)[:L].sum()) for t in types]
+    L_cap = max(L, max(keep_n) + steps)
+    meta = P().SpanMeta(spans, T, DEV)
+    cache = P().KVCache(M, b, H, L_cap, d, torch.bfloat16, DEV)
+    ws = P().Workspace(b, H, L, L_cap, d, DEV)
+    for m in range(M):
+        for kv in range(2):
+            cache.kv[m, kv, :, :, :L].copy_(
+                W().randn((b, H, L, d), seed=w.seed * 1000 + 2 * m + kv, device=DEV))
+    cache.start_prompt(L, meta)
+    checks = 0
+    if prefill_layer is not None:
+        m = prefill_layer
+        qi, ki = (W().randn((b, H, L, d), seed=w.seed * 1000 + 900 + i, device=DEV) for i in range(2))
+        qr = torch.empty_like(qi)
+        P().rope_rows(qi, qr, meta, L, 0, theta)
+        P().rope_rows(ki, cache.k(m), meta, L, 0, theta)
+        o = torch.empty_like(qi)
+        P().prefill_layer(qr, cache.k(m), cache.v(m), o, meta, ws, L)
+        torch.cuda.synchronize()
+        for s, h in prefill_heads:
+            say(f"  prefill oracle s={s} h={h}")
+            Q, K = f64(qi[s, h]), f64(ki[s, h])
+            if theta > 0:
+                Q = O.rope_rotate_half(Q, pos[s][:L], theta)
+                K = O.rope_rotate_half(K, pos[s][:L], theta)
+            mask = O.attention_mask(types[s][:L])
+            ref = O.masked_attention(Q[None], K[None], f64(cache.v(m)[s, h, :L])[None], mask)[0]
+            assert np.abs(f64(o[s, h]) - ref).max() <= TOL
+            checks += 1
+    before = {(m, s, h): (f64(cache.kv[m, 0, s, h, :L]), f64(cache.kv[m, 1, s, h, :L]))
+              for m, s, h in samples}
+    cache.compact(meta)
+    torch.cuda.synchronize()
+    assert cache.kv_len.tolist() == keep_n
+    for s in range(b):
+        ref = O.compact_cache(np.zeros((1, L, 1)), np.zeros((1, L, 1)), np.arange(L),
+                              pos[s][:L].copy(), L, types[s], L)
+        assert np.array_equal(cache.tok_idx[s, :keep_n[s]].cpu().numpy(), ref[2][:keep_n[s]])
+        assert np.array_equal(cache.pos_ids[s, :keep_n[s]].cpu().numpy(), ref[3][:keep_n[s]])
+        assert np.array_equal(cache.kept_src[s, :keep_n[s]].cpu().numpy(), ref[5])
+    for (m, s, h), (K0, V0) in before.items():
+        ks = cache.kept_src[s, :keep_n[s]].cpu().numpy()
+        assert np.array_equal(f64(cache.kv[m, 0, s, h, :keep_n[s]]), K0[ks])
+        assert np.array_equal(f64(cache.kv[m, 1, s, h, :keep_n[s]]), V0[ks])
+    POOL = 8
+    qd = W().randn((POOL, M, b, H, d), seed=w.seed * 1000 + 501, device=DEV)
+    kd = W().randn((POOL, M, b, H, d), seed=w.seed * 1000 + 502, device=DEV)
+    vd = W().randn((POOL, M, b, H, d), seed=w.seed * 1000 + 503, device=DEV)
+    cr_steps = sorted({r for s in spans for _, r in s if L <= r < T})
+    got = {k: {} for k in samples}
+    od = torch.empty(b, H, d, dtype=torch.bfloat16, device=DEV)
+    for i in range(steps):
+        for m in range(M):
+            P().decode_layer(qd[i % POOL, m], kd[i % POOL, m], vd[i % POOL, m], cache, m, meta,
+                             ws, od, theta=theta)
+            if i + 1 in check:
+                for (mm, s, h) in samples:
+                    if mm == m:
+                        got[(m, s, h)][i + 1] = f64(od[s, h])
+        cache.commit(meta)
+        if L + i in cr_steps:
+            cache.compact(meta)
+    torch.cuda.synchronize()
+    assert int(cache.status) == 0
+    Q, K, V = f64(qd), f64(kd), f64(vd)
+    for (m, s, h), (K0, V0) in before.items():
+        say(f"  decode oracle m={m} s={s} h={h}")
+        idx = [i % POOL for i in range(steps)]
+        ref = oracle_slice(K0, V0, L, types[s], pos[s], Q[idx, m, s, h], K[idx, m, s, h],
+                           V[idx, m, s, h], theta, set(cr_steps), check)
+        for st in check:
+            err = np.abs(got[(m, s, h)][st] - ref[st]).max()
+            assert err <= TOL, (m, s, h, st, err)
+            checks += 1
+    return checks
+
+
+def test_fullsize_3b_rope_prefill_compact_decode():
+    """32 layers, b=16, H=32, d=80, L=4096, 50% freed, rotary, 128 steps."""
+    w = W().get_workload("3b-rope")
+    say(f"full size {w.name}")
+    rng = np.random.default_rng(4)
+    samples = [(int(rng.integers(w.layers)), int(rng.integers(w.batch)), int(rng.integers(w.heads)))
+               for _ in range(4)] + [(5, 3, 7)]
+    n = run_decode_workload(w, w.decode_steps, samples, check={1, 64, 128}, prefill_layer=5,
+                            prefill_heads=[(3, 7), (11, 30)])
+    assert n == 2 + 3 * len(samples)
+
+
+def test_fullsize_opt13b_compact_decode():
+    """24 layers, b=64, H=32, d=64, L=2048, 75% freed, 128 steps."""
+    w = W().get_workload("opt1.3b-decode")
+    say(f"full size {w.name}")
+    rng = np.random.default_rng(3)
+    samples = [(int(rng.integers(w.layers)), int(rng.integers(w.batch)), int(rng.integers(w.heads)))
+               for _ in range(5)]
+    run_decode_workload(w, w.decode_steps, samples, check={1, 64, 128})
+
+
+def test_fullsize_streaming_batch256_short():
+    """The streaming workload at full batch (b=256, 32 layers, d=80, prompt
+    1024) for its first 120 generated tokens (two spans close)."""
+    w = W().get_workload("3b-rope-stream")
+    say(f"full size {w.name} (120 generated tokens)")
+    rng = np.random.default_rng(5)
+    samples = [(int(rng.integers(w.layers)), int(rng.integers(w.batch)), int(rng.integers(w.heads)))
+               for _ in range(4)]
+    run_decode_workload(w, 120, samples, check={1, 40, 41, 65, 120})

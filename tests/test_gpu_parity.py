@@ -413,14 +413,30 @@ def test_decode_reports_capacity_and_token_errors():
 # the whole path on a small RoPE model: masked full cache == compacted cache
 # ---------------------------------------------------------------------------
 
-@pytest.mark.parametrize("dtype,d,theta", [("bf16", 80, 10000.0), ("f32", 64, 0.0)])
-def test_end_to_end_prompt_compact_decode(dtype, d, theta):
-    say(f"end to end dtype={dtype} d={d}")
+E2E_CASES = {
+    # prompt spans, spans crossing the prompt end, spans closing mid-generation
+    "mixed-bf16-rope": ("bf16", 80, 10000.0, 300, 100,
+                        [[(10, 50), (51, 52), (120, 250), (290, 330), (340, 341), (345, 380),
+                          (390, 420)],
+                         [(0, 299), (305, 340), (360, 361)]]),
+    "mixed-f32": ("f32", 64, 0.0, 300, 100,
+                  [[(10, 50), (51, 52), (120, 250), (290, 330), (340, 341), (345, 380),
+                    (390, 420)],
+                   [(0, 299), (305, 340), (360, 361)]]),
+    # the streaming schedule: no prompt spans, <CL> at +8 and <CR> at +40 of
+    # every 48 generated tokens, compaction right after each <CR>
+    "streaming-bf16-rope": ("bf16", 80, 10000.0, 64, 200, "stream"),
+}
+
+
+@pytest.mark.parametrize("case", list(E2E_CASES))
+def test_end_to_end_prompt_compact_decode(case):
+    dtype, d, theta, L, steps, spans = E2E_CASES[case]
+    say(f"end to end case={case}")
     M, b, H = 2, 2, 2
-    L, steps = 300, 100
     T = L + steps
-    spans = [[(10, 50), (51, 52), (120, 250), (290, 330), (340, 341), (345, 380), (390, 420)],
-             [(0, 299), (305, 340), (360, 361)]]
+    if spans == "stream":
+        spans = [W().spans_streaming(L, steps, 48, 8, 40) for _ in range(b)]
     types = [O.token_types(sp, T) for sp in spans]
     cr_steps = sorted({r for sp in spans for _, r in sp if L <= r < T})
     q, k, v = (rnd((M, b, H, T, d), 300 + i, dtype) for i in range(3))
