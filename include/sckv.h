@@ -192,7 +192,7 @@ int kv_compact(void* kv, void* kv_out, int32_t M, int32_t b, int32_t H, int32_t 
  *          holding the split-K partials (overwritten; calls that share a
  *          workspace must be ordered, e.g. enqueued on one stream).
  * status : nullable int32, status bits OR-ed in.
- * The key rows are split into chunks of 256 rows, one workgroup each; a
+ * The key rows are split into chunks of 1024 rows, one workgroup each; a
  * second kernel merges the chunk partials (log-sum-exp) into o.
  * ------------------------------------------------------------------------- */
 size_t sckv_decode_workspace_bytes(int32_t b, int32_t H, int32_t L_cap, int32_t d_head);

@@ -3,7 +3,8 @@
 // cost) and Section 4.3 (generation continues from the compressed cache).
 //
 // decode_chunk_kernel : one workgroup per (sequence, head, chunk of CH rows),
-//   in an XCD-aware order so that the chunks of one slice share an L2.  A
+//   chunk-major (chunks of one slice share no data but q, so L2 placement
+//   does not matter; idle workgroups past a slice's end go last).  A
 //   workgroup streams its rows with a 16-byte piece per lane; a row is spread
 //   over LPR lanes of an aligned power-of-two group of GRP lanes, so the row
 //   dot product is a DPP butterfly inside the group.  Each lane group keeps an
@@ -23,8 +24,11 @@
 
 namespace sckv {
 
+// Tuning (measured on MI355X over the OPT-1.3B, 3B-RoPE and batch-256
+// streaming decode shapes): 1024-row chunks, 4 rows per lane group in flight
+// per trip, 256 threads, chunk-major dispatch order.
 constexpr int DEC_THREADS = 256;
-constexpr int DEC_CH = 256;  // rows per chunk
+constexpr int DEC_CH = 1024;  // rows per chunk (one workgroup)
 constexpr float LOG2E = 1.4426950408889634f;
 
 struct RopeTab {
@@ -37,7 +41,7 @@ struct DecCfg {
   static constexpr int LPR = D / E;               // pieces per row
   static constexpr int GRP = LPR <= 8 ? 8 : (LPR <= 16 ? 16 : 32);
   static constexpr int RPW = 64 / GRP;            // rows per wave per step
-  static constexpr int U = 4;                     // steps per trip
+  static constexpr int U = 4;                     // steps per trip (loads in flight per lane: 2U)
   static constexpr int NG = (DEC_THREADS / 64) * RPW;  // lane groups per workgroup
 };
 
@@ -55,11 +59,12 @@ __device__ __forceinline__ void load_rotated_piece(const T* x, int seg, bool rot
   float partner[E];
   Piece<T>::unpack(ld16(x + pseg * E), partner);
   const double two_pi = 6.283185307179586476925286766559;
+  const double inv_two_pi = 0.15915494309189533576888376337251;
   const int i0 = (first ? seg : pseg) * E;
 #pragma unroll
   for (int e = 0; e < E; ++e) {
     double ang = ps * inv[i0 + e];
-    ang -= two_pi * rint(ang / two_pi);
+    ang -= two_pi * rint(ang * inv_two_pi);
     float sn, cs;
     sincosf((float)ang, &sn, &cs);
     out[e] = first ? out[e] * cs - partner[e] * sn : out[e] * cs + partner[e] * sn;
@@ -87,12 +92,12 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_chunk_kernel(
     int rotate, RopeTab tab, float* __restrict__ part, int32_t n_chunk_max, int32_t n_work) {
   using C = DecCfg<T, D>;
   constexpr int E = C::E, LPR = C::LPR, GRP = C::GRP, RPW = C::RPW, U = C::U, NG = C::NG;
-  const int x = blockIdx.x;
-  const int xcd = x & 7, idx = x >> 3;
-  const int qn = n_work >> 3, rem = n_work & 7;
-  const int work = xcd * qn + min(xcd, rem) + idx;
-  const int bh = work / n_chunk_max;
-  const int chunk = work % n_chunk_max;
+  // chunk-major order: every slice's first chunk is dispatched before any
+  // slice's second chunk, so the workgroups that start past a slice's last
+  // row (and exit at once) are dispatched last
+  const int n_bh = n_work / n_chunk_max;
+  const int chunk = blockIdx.x / n_bh;
+  const int bh = blockIdx.x % n_bh;
   const int s = bh / H;
   if (step_kind(cur_tok, vu, kv_len, s, L_meta, L_cap) != 0) return;  // combine handles it
   const int n = kv_len[s];
@@ -109,6 +114,26 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_chunk_kernel(
   const int seg = lane % GRP;    // piece within the row
   const bool active = seg < LPR;
 
+  const T* kb = k_cache + (int64_t)bh * L_cap * D;
+  const T* vb = v_cache + (int64_t)bh * L_cap * D;
+  constexpr int TRIP = (DEC_THREADS / 64) * U * RPW;  // rows per trip of the workgroup
+  const int base0 = r0 + wave * U * RPW;
+
+  // streamed rows: the 2U loads of one trip are issued together
+  u32x4 kw[U], vw[U];
+  auto issue = [&](int base, u32x4* kd, u32x4* vd) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int row = base + u * RPW + g;
+      if (row < rc && active) {
+        kd[u] = ld16(kb + (int64_t)row * D + seg * E);
+        vd[u] = ld16(vb + (int64_t)row * D + seg * E);
+      } else {
+        kd[u] = u32x4{0, 0, 0, 0};
+        vd[u] = u32x4{0, 0, 0, 0};
+      }
+    }
+  };
   __shared__ double inv[D / 2];
   if (rotate && tid < D / 2) inv[tid] = tab.w[tid];
   __syncthreads();
@@ -123,28 +148,12 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_chunk_kernel(
     for (int e = 0; e < E; ++e) qf[e] *= qscale;  // scores come out in log2 units
   }
 
-  const T* kb = k_cache + (int64_t)bh * L_cap * D;
-  const T* vb = v_cache + (int64_t)bh * L_cap * D;
   float m = -INFINITY, l = 0.f, acc[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) acc[e] = 0.f;
 
-  constexpr int TRIP = (DEC_THREADS / 64) * U * RPW;  // rows per trip
-  for (int base = r0 + wave * U * RPW; base < rc; base += TRIP) {
-    u32x4 kw[U], vw[U];
-    bool ok[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int row = base + u * RPW + g;
-      ok[u] = row < rc;
-      if (ok[u] && active) {
-        kw[u] = ld16(kb + (int64_t)row * D + seg * E);
-        vw[u] = ld16(vb + (int64_t)row * D + seg * E);
-      } else {
-        kw[u] = u32x4{0, 0, 0, 0};
-        vw[u] = u32x4{0, 0, 0, 0};
-      }
-    }
+  issue(base0, kw, vw);
+  for (int base = base0; base < rc; base += TRIP) {
     float sc[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -154,7 +163,7 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_chunk_kernel(
 #pragma unroll
       for (int e = 0; e < E; ++e) d = fmaf(qf[e], kf[e], d);
       d = group_sum<GRP>(d);
-      sc[u] = ok[u] ? d : -INFINITY;
+      sc[u] = (base + u * RPW + g < rc) ? d : -INFINITY;
     }
     float mx = m;
 #pragma unroll
@@ -175,6 +184,7 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_chunk_kernel(
       }
       m = mx;
     }
+    if (base + TRIP < rc) issue(base + TRIP, kw, vw);
   }
 
   // the new row: rotated k_new, v_new; written to the cache by this chunk
@@ -246,30 +256,53 @@ __global__ __launch_bounds__(128) void decode_combine_kernel(
   if (kind >= 2 && tid == 0 && (bh % H) == 0 && status)
     atomicOr(status, kind == 2 ? SCKV_STATUS_TOKEN : SCKV_STATUS_CAP);
   __shared__ float res[D];
-  if (tid < D) {
-    float r;
-    if (kind == 1) {
-      const T* vn = v_new + (int64_t)bh * D;
-      if constexpr (sizeof(T) == 2) r = bf16_lo((uint32_t)vn[tid]);
-      else r = vn[tid];
-    } else if (kind != 0) {
-      r = NAN;
-    } else {
-      const int nch = (kv_len[s] + 1 + DEC_CH - 1) / DEC_CH;
-      const float* p = part + (int64_t)bh * n_chunk_max * (D + 2);
-      float M = -INFINITY;
-      for (int c = 0; c < nch; ++c) M = fmaxf(M, p[c * (D + 2)]);
-      float Lsum = 0.f, acc = 0.f;
-      for (int c = 0; c < nch; ++c) {
-        const float mc = p[c * (D + 2)];
-        if (mc == -INFINITY) continue;
-        const float w = exp2f(mc - M);
-        Lsum += p[c * (D + 2) + 1] * w;
-        acc += p[c * (D + 2) + 2 + tid] * w;
+  __shared__ float cw[128];  // chunk weights exp2(m_c - M), a block of 128 chunks at a time
+  __shared__ float red[2];
+  if (kind != 0) {
+    if (tid < D) {
+      float r = NAN;
+      if (kind == 1) {
+        const T* vn = v_new + (int64_t)bh * D;
+        if constexpr (sizeof(T) == 2) r = bf16_lo((uint32_t)vn[tid]);
+        else r = vn[tid];
       }
-      r = acc / Lsum;
+      res[tid] = r;
     }
-    res[tid] = r;
+  } else {
+    const int nch = (kv_len[s] + 1 + DEC_CH - 1) / DEC_CH;
+    const float* p = part + (int64_t)bh * n_chunk_max * (D + 2);
+    // global max over the chunk maxima (one wave)
+    if (tid < 64) {
+      float M = -INFINITY;
+      for (int c = tid; c < nch; c += 64) M = fmaxf(M, p[c * (D + 2)]);
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) M = fmaxf(M, __shfl_xor(M, off, 64));
+      if (tid == 0) red[0] = M;
+    }
+    __syncthreads();
+    const float M = red[0];
+    float Lsum = 0.f, acc = 0.f;
+    for (int c0 = 0; c0 < nch; c0 += 128) {
+      const int c = c0 + tid;
+      if (c < nch) {
+        const float mc = p[c * (D + 2)];
+        const float w = (mc == -INFINITY) ? 0.f : exp2f(mc - M);
+        cw[tid] = w;
+      }
+      __syncthreads();
+      const int cn = min(128, nch - c0);
+      if (tid < D) {
+#pragma unroll 8
+        for (int i = 0; i < cn; ++i) {
+          const float w = cw[i];
+          const float* pc = p + (c0 + i) * (D + 2);
+          Lsum = fmaf(pc[1], w, Lsum);
+          acc = fmaf(pc[2 + tid], w, acc);
+        }
+      }
+      __syncthreads();
+    }
+    if (tid < D) res[tid] = acc / Lsum;
   }
   __syncthreads();
   if (tid < D / E) {

@@ -102,7 +102,7 @@ def test_compact_rejects(B):
 def test_decode_rejects(B):
     f = B.lib.compacted_decode_attn
     ws = B.lib.sckv_decode_workspace_bytes(2, 4, 512, 80)
-    assert ws == 2 * 4 * 2 * 82 * 4
+    assert ws == 2 * 4 * 1 * 82 * 4  # one 1024-row chunk per (sequence, head)
     def call(**kw):
         a = dict(d=80, dt=B.BF16, scale=0.1, theta=0.0, ws=ws, pos=FAKE, b=2, H=4, Lc=512)
         a.update(kw)
@@ -113,7 +113,7 @@ def test_decode_rejects(B):
     assert call(theta=-1.0) == B.EINVAL
     assert call(theta=1e4, pos=NULL) == B.EINVAL
     assert call(scale=float("nan")) == B.EINVAL
-    assert call(b=1 << 28) == B.EUNSUP
+    assert call(b=1 << 30) == B.EUNSUP
 
 
 def test_rope_and_commit_reject(B):
