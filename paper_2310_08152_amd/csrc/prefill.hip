@@ -34,6 +34,11 @@ constexpr int PF_BK = 64;
 constexpr int PF_THREADS = 256;
 constexpr uint32_t PF_NONE = 0x00ffffffu;  // list entry of a padding column
 constexpr float PF_LOG2E = 1.4426950408889634f;
+// The running maximum of a query row is only moved (and the accumulators
+// rescaled) when a tile's maximum exceeds it by more than this many powers of
+// two; until then probabilities are taken relative to the older, smaller
+// maximum, which is exact and keeps them below 2^PF_RESCALE.
+constexpr float PF_RESCALE = 8.f;
 
 __global__ __launch_bounds__(256) void prefill_plan_kernel(const int32_t* __restrict__ vu,
                                                            int32_t L_meta, int32_t L, int32_t n_qt,
@@ -84,11 +89,15 @@ template <typename T, int D> struct PfCfg;
 
 template <int D> struct PfCfg<uint16_t, D> {
   static constexpr int NBUF = 2;
-  static constexpr int DP = (D + 31) / 32 * 32;     // value rows padded to whole 32-row MFMA blocks
+  static constexpr int DP = (D + 31) / 32 * 32;     // value columns padded to whole 32-row MFMA blocks
   static constexpr int KP = D + 8;                  // K tile: [64][KP] bf16
-  static constexpr int VP = PF_BK + 4;              // V^T tile: [DP][VP] bf16
+  // V tile: [64][VP] bf16, row-major like K; the PV operand is read with the
+  // transposing LDS read.  A 192-byte pitch puts the four rows one
+  // transposing read touches in disjoint groups of 16 banks.
+  static constexpr int VP = 96;
+  static_assert(DP <= VP, "value tile pitch");
   static constexpr int KBYTES = PF_BK * KP * 2;
-  static constexpr int VBYTES = DP * VP * 2;
+  static constexpr int VBYTES = PF_BK * VP * 2;
   static constexpr int PPR = D / 8;                 // 16-byte pieces per row
   static constexpr int KSTEPS = D / 16;
 };
@@ -108,13 +117,15 @@ struct TileInfo {
   int jmin, jmax, vrmin, nvalid;
 };
 
+constexpr int PF_ER = 4;  // ring of list entries: tile kt+2 is fetched while kt is computed
+
 template <typename T, int D>
 struct PfSmem {
   using C = PfCfg<T, D>;
   char k[C::NBUF][C::KBYTES];
   char v[C::NBUF][C::VBYTES];
-  uint32_t ent[C::NBUF][PF_BK];
-  TileInfo info[C::NBUF];
+  uint32_t ent[PF_ER][PF_BK];
+  TileInfo info[PF_ER];
 };
 
 // ---------------------------------------------------------------------------
@@ -162,12 +173,18 @@ __global__ __launch_bounds__(PF_THREADS, 2) void prefill_attn_kernel(
   const int n_vis = count[(int64_t)s * n_qt + qt];
   const int nt = (n_vis + PF_BK - 1) / PF_BK;
 
-  // zero the padding value rows/columns once (never written afterwards)
+  // Padding value rows/columns are written once and never again.  For bf16
+  // with padding, V^T row D is all ones, so the PV MFMA also produces each
+  // query's probability sum (O^T row D) and no separate row sum is needed.
+  constexpr bool ONES_SUM = BF && (C::DP != D);
   if constexpr (C::DP != D) {
     for (int b = 0; b < C::NBUF; ++b) {
       if constexpr (BF) {
-        uint16_t* vt = reinterpret_cast<uint16_t*>(sm.v[b]);
-        for (int i = tid; i < (C::DP - D) * C::VP; i += PF_THREADS) vt[D * C::VP + i] = 0;
+        uint16_t* vs = reinterpret_cast<uint16_t*>(sm.v[b]);
+        for (int i = tid; i < PF_BK * (C::DP - D); i += PF_THREADS) {
+          const int c = D + i % (C::DP - D);
+          vs[(i / (C::DP - D)) * C::VP + c] = (c == D) ? (uint16_t)0x3f80 : (uint16_t)0;
+        }
       } else {
         float* vs = reinterpret_cast<float*>(sm.v[b]);
         for (int i = tid; i < PF_BK * (C::DP - D); i += PF_THREADS)
@@ -196,12 +213,37 @@ __global__ __launch_bounds__(PF_THREADS, 2) void prefill_attn_kernel(
     for (int i = 0; i < 16; ++i) oacc[db][i] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
 
-  // ---- staging of one gathered tile: global -> registers -> LDS ----
+  // ---- staging: list entries run two tiles ahead through an LDS ring, so
+  // the key/value rows of tile kt+1 are addressed from LDS and their loads
+  // are in flight while tile kt is multiplied ----
   u32x4 kreg[PPT], vreg[PPT];
   uint32_t ereg = PF_NONE;
-  auto load_tile = [&](int kt) {
-    const int base = kt * PF_BK;
-    const int nvalid = min(PF_BK, n_vis - base);
+  auto nvalid_of = [&](int kt) { return min(PF_BK, n_vis - kt * PF_BK); };
+  auto load_entries = [&](int kt) {
+    ereg = (tid < PF_BK && tid < nvalid_of(kt)) ? ents[kt * PF_BK + tid] : PF_NONE;
+  };
+  auto store_entries = [&](int kt) {
+    const int slot = kt % PF_ER;
+    if (tid < 64) {
+      const int nvalid = nvalid_of(kt);
+      sm.ent[slot][tid] = ereg;
+      int vr = (tid < nvalid) ? (int)(ereg >> 24) : 255;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) vr = min(vr, __shfl_xor(vr, off, 64));
+      const int jmax = __shfl((int)(ereg & 0x00ffffffu), nvalid - 1, 64);
+      if (tid == 0) {
+        TileInfo ti;
+        ti.jmin = (int)(ereg & 0x00ffffffu);
+        ti.jmax = jmax;
+        ti.vrmin = vr;
+        ti.nvalid = nvalid;
+        sm.info[slot] = ti;
+      }
+    }
+  };
+  auto load_rows = [&](int kt) {  // entries of tile kt are in the ring
+    const int slot = kt % PF_ER;
+    const int nvalid = nvalid_of(kt);
 #pragma unroll
     for (int p = 0; p < PPT; ++p) {
       const int piece = p * PF_THREADS + tid;
@@ -209,16 +251,13 @@ __global__ __launch_bounds__(PF_THREADS, 2) void prefill_attn_kernel(
       kreg[p] = u32x4{0, 0, 0, 0};
       vreg[p] = u32x4{0, 0, 0, 0};
       if (piece < NPIECE && r < nvalid) {
-        const int j = (int)(ents[base + r] & 0x00ffffffu);
+        const int j = (int)(sm.ent[slot][r] & 0x00ffffffu);
         kreg[p] = ld16(kb + (int64_t)j * D + sg * Piece<T>::E);
         vreg[p] = ld16(vb + (int64_t)j * D + sg * Piece<T>::E);
       }
     }
-    ereg = (tid < nvalid) ? ents[base + tid] : PF_NONE;
   };
-  auto store_tile = [&](int kt, int buf) {
-    const int base = kt * PF_BK;
-    const int nvalid = min(PF_BK, n_vis - base);
+  auto store_rows = [&](int buf) {
 #pragma unroll
     for (int p = 0; p < PPT; ++p) {
       const int piece = p * PF_THREADS + tid;
@@ -226,12 +265,7 @@ __global__ __launch_bounds__(PF_THREADS, 2) void prefill_attn_kernel(
       const int r = piece / PPR, sg = piece % PPR;
       if constexpr (BF) {
         *reinterpret_cast<u32x4*>(sm.k[buf] + (r * C::KP + sg * 8) * 2) = kreg[p];
-        uint16_t* vt = reinterpret_cast<uint16_t*>(sm.v[buf]);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          vt[(sg * 8 + 2 * e) * C::VP + r] = (uint16_t)(vreg[p][e] & 0xffffu);
-          vt[(sg * 8 + 2 * e + 1) * C::VP + r] = (uint16_t)(vreg[p][e] >> 16);
-        }
+        *reinterpret_cast<u32x4*>(sm.v[buf] + (r * C::VP + sg * 8) * 2) = vreg[p];
       } else {
         float* ks = reinterpret_cast<float*>(sm.k[buf]) + r * C::KP + sg * 4;
 #pragma unroll
@@ -239,31 +273,26 @@ __global__ __launch_bounds__(PF_THREADS, 2) void prefill_attn_kernel(
         *reinterpret_cast<u32x4*>(sm.v[buf] + (r * C::VP + sg * 4) * 4) = vreg[p];
       }
     }
-    if (tid < 64) {
-      sm.ent[buf][tid] = ereg;
-      int vr = (tid < nvalid) ? (int)(ereg >> 24) : 255;
-#pragma unroll
-      for (int off = 1; off < 64; off <<= 1) vr = min(vr, __shfl_xor(vr, off, 64));
-      if (tid == 0) {
-        TileInfo ti;
-        ti.jmin = (int)(ereg & 0x00ffffffu);
-        ti.jmax = (int)(ents[base + nvalid - 1] & 0x00ffffffu);
-        ti.vrmin = vr;
-        ti.nvalid = nvalid;
-        sm.info[buf] = ti;
-      }
-    }
   };
 
-  load_tile(0);
-  store_tile(0, 0);
+  load_entries(0);
+  store_entries(0);
+  if (nt > 1) {
+    load_entries(1);
+    store_entries(1);
+  }
+  __syncthreads();
+  load_rows(0);
+  store_rows(0);
   __syncthreads();
 
   for (int kt = 0; kt < nt; ++kt) {
     const int cur = kt % C::NBUF;
-    if (kt + 1 < nt) load_tile(kt + 1);
+    if (kt + 2 < nt) load_entries(kt + 2);
+    if (kt + 1 < nt) load_rows(kt + 1);
 
-    const TileInfo ti = sm.info[cur];
+    const TileInfo ti = sm.info[kt % PF_ER];
+    const uint32_t* tent = sm.ent[kt % PF_ER];
     if (wave_live && ti.jmin <= Iw + 31) {
       const bool full = ti.nvalid == PF_BK && ti.jmax <= Iw && ti.vrmin >= Iw + 31 - I;
       // ---- S^T = K Q^T for the two 32-key blocks ----
@@ -294,37 +323,40 @@ __global__ __launch_bounds__(PF_THREADS, 2) void prefill_attn_kernel(
 #pragma unroll
           for (int vv = 0; vv < 16; ++vv) {
             const int key = kb2 * 32 + 8 * (vv >> 2) + 4 * g + (vv & 3);
-            const uint32_t e = sm.ent[cur][key];
+            const uint32_t e = tent[key];
             const int j = (int)(e & 0x00ffffffu);
             const int vr = (int)(e >> 24);
             if (!(j <= qrow && ir <= vr)) sacc[kb2][vv] = -INFINITY;
           }
       }
-      // ---- online softmax (log2 units) ----
+      // ---- online softmax (log2 units), lazy rescaling ----
       float mx = -INFINITY;
 #pragma unroll
       for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
         for (int vv = 0; vv < 16; ++vv) mx = fmaxf(mx, sacc[kb2][vv]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float m_new = fmaxf(m_run, mx * c2);
-      const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-      const float alpha = exp2f(m_run - m_use);
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c2;
+      const bool grow = mx > m_run + PF_RESCALE;
+      if (__ballot(grow) != 0) {
+        const float alpha = grow ? fast_exp2(m_run - mx) : 1.f;  // m_run == -inf gives 0
+        if (grow) m_run = mx;
+        l_run *= alpha;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
+      }
+      const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
       float rs = 0.f;
 #pragma unroll
       for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
         for (int vv = 0; vv < 16; ++vv) {
-          const float p = exp2f(fmaf(sacc[kb2][vv], c2, -m_use));
+          const float p = fast_exp2(fmaf(sacc[kb2][vv], c2, -m_use));
           sacc[kb2][vv] = p;
-          rs += p;
+          if constexpr (!ONES_SUM) rs += p;
         }
-      l_run = l_run * alpha + rs;
-      m_run = m_new;
-#pragma unroll
-      for (int db = 0; db < NDB; ++db)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
+      if constexpr (!ONES_SUM) l_run += rs;
       // ---- O^T += V^T P^T ----
       if constexpr (BF) {
         bf16x8 pb[4];
@@ -336,15 +368,19 @@ __global__ __launch_bounds__(PF_THREADS, 2) void prefill_attn_kernel(
             w[i] = pack_bf16x2(sacc[t >> 1][8 * (t & 1) + 2 * i], sacc[t >> 1][8 * (t & 1) + 2 * i + 1]);
           pb[t] = __builtin_bit_cast(bf16x8, w);
         }
-        const uint16_t* vt = reinterpret_cast<const uint16_t*>(sm.v[cur]);
+        // A operand V^T[d][keys]: within each group of 16 lanes, lane j points
+        // at V[kbase + j/4][dbase + 4*(j%4)]; the transposing read hands lane
+        // i the four keys kbase..kbase+3 of column dbase + i.
+        const uint16_t* vs = reinterpret_cast<const uint16_t*>(sm.v[cur]);
+        const int G = lane >> 4, j16 = lane & 15;
+        const uint16_t* vsrc = vs + (4 * g + (j16 >> 2)) * C::VP + 16 * (G & 1) + 4 * (j16 & 3);
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {
-          const uint16_t* vrow = vt + (db * 32 + l32) * C::VP + 4 * g;
 #pragma unroll
           for (int t = 0; t < 4; ++t) {
-            const u32x2 lo = *reinterpret_cast<const u32x2*>(vrow + 16 * t);
-            const u32x2 hi = *reinterpret_cast<const u32x2*>(vrow + 16 * t + 8);
-            const u32x4 w = u32x4{lo[0], lo[1], hi[0], hi[1]};
+            const s16x4 lo = lds_read_tr16(vsrc + (16 * t) * C::VP + 32 * db);
+            const s16x4 hi = lds_read_tr16(vsrc + (16 * t + 8) * C::VP + 32 * db);
+            const s16x8 w = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
             oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, w), pb[t],
                                                                oacc[db], 0, 0, 0);
           }
@@ -365,13 +401,21 @@ __global__ __launch_bounds__(PF_THREADS, 2) void prefill_attn_kernel(
     }
 
     if constexpr (C::NBUF == 1) __syncthreads();
-    if (kt + 1 < nt) store_tile(kt + 1, (kt + 1) % C::NBUF);
+    if (kt + 1 < nt) store_rows((kt + 1) % C::NBUF);
+    if (kt + 2 < nt) store_entries(kt + 2);
     __syncthreads();
   }
 
   // ---- epilogue: normalise and write; a <CL> row copies its value row ----
   if (!wave_live) return;
-  const float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+  float l_tot;
+  if constexpr (ONES_SUM) {
+    // O^T row D sits in d-block D/32, accumulator 8*((D%32)/8) of lane group 0
+    static_assert((D % 32) % 8 == 0, "ones row must start a group of 8 rows");
+    l_tot = __shfl(oacc[D / 32][4 * ((D % 32) / 8)], l32, 64);
+  } else {
+    l_tot = l_run + __shfl_xor(l_run, 32, 64);
+  }
   if (qrow >= L) return;
   const float inv = 1.f / l_tot;
   const bool is_cl = vu[(int64_t)s * L_meta + qrow] == qrow;

@@ -75,6 +75,20 @@ template <> struct Piece<float> {
   }
 };
 
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+
+// 2^x with the hardware instruction; results below 2^-126 flush to zero,
+// which is what a softmax weight of that size contributes anyway
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// ds_read_b64_tr_b16 (gfx950): inside each group of 16 lanes, lane i gets
+// element e = (the 4 halves at lane 4e + i/4's address)[i % 4]
+__device__ __forceinline__ s16x4 lds_read_tr16(const void* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) s16x4*)(const_cast<void*>(p)));
+}
+
 __device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
 __device__ __forceinline__ void st16(void* p, const u32x4& v) { *reinterpret_cast<u32x4*>(p) = v; }
 
