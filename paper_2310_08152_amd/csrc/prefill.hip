@@ -326,7 +326,8 @@ __global__ __launch_bounds__(PF_THREADS, 2) void prefill_attn_kernel(
             const uint32_t e = tent[key];
             const int j = (int)(e & 0x00ffffffu);
             const int vr = (int)(e >> 24);
-            if (!(j <= qrow && ir <= vr)) sacc[kb2][vv] = -INFINITY;
+            const bool vis = (j <= qrow) & (ir <= vr);
+            sacc[kb2][vv] = vis ? sacc[kb2][vv] : -INFINITY;
           }
       }
       // ---- online softmax (log2 units), lazy rescaling ----
