@@ -131,8 +131,10 @@ struct PfSmem {
 // ---------------------------------------------------------------------------
 // main kernel
 // ---------------------------------------------------------------------------
+// Three waves per SIMD (at most 168 registers) measured faster than two
+// (more room for the register-hungry d=80 tiles) and than four.
 template <typename T, int D>
-__global__ __launch_bounds__(PF_THREADS, 2) void prefill_attn_kernel(
+__global__ __launch_bounds__(PF_THREADS) __attribute__((amdgpu_waves_per_eu(3))) void prefill_attn_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v, T* __restrict__ o,
     int32_t H, int32_t L, int64_t qs, int64_t kvs, int64_t os, float c2,
     const int32_t* __restrict__ vu, int32_t L_meta, const uint32_t* __restrict__ list,
