@@ -90,27 +90,37 @@ template <typename T, int D> struct PfCfg;
 template <int D> struct PfCfg<uint16_t, D> {
   static constexpr int NBUF = 2;
   static constexpr int DP = (D + 31) / 32 * 32;     // value columns padded to whole 32-row MFMA blocks
-  static constexpr int KP = D + 8;                  // K tile: [64][KP] bf16
+  static constexpr int KP = D + 8;                  // K tile: [64][KP] bf16 (one 16-byte pad slot)
   // V tile: [64][VP] bf16, row-major like K; the PV operand is read with the
   // transposing LDS read.  A 192-byte pitch puts the four rows one
   // transposing read touches in disjoint groups of 16 banks.
   static constexpr int VP = 96;
   static_assert(DP <= VP, "value tile pitch");
-  static constexpr int KBYTES = PF_BK * KP * 2;
-  static constexpr int VBYTES = PF_BK * VP * 2;
-  static constexpr int PPR = D / 8;                 // 16-byte pieces per row
+  static constexpr int E = 8;                       // elements per 16-byte slot
   static constexpr int KSTEPS = D / 16;
 };
 
 template <int D> struct PfCfg<float, D> {
   static constexpr int NBUF = 1;
   static constexpr int DP = (D + 31) / 32 * 32;
-  static constexpr int KP = D + 2;                  // K tile: [64][KP] f32
+  static constexpr int KP = D + 4;                  // K tile: [64][KP] f32
   static constexpr int VP = DP + 8;                 // V tile: [64][VP] f32 (row-major)
-  static constexpr int KBYTES = PF_BK * KP * 4;
-  static constexpr int VBYTES = PF_BK * VP * 4;
-  static constexpr int PPR = D / 4;
+  static constexpr int E = 4;
   static constexpr int KSTEPS = D / 2;
+};
+
+// Row slots of a staged tile.  Rows are copied global -> LDS by the
+// direct-to-LDS load (16 bytes per lane, lane i of an instruction writes
+// slot base+i), so a tile is a whole number of 1 KiB blocks of 64 slots.
+template <typename T, int D>
+struct PfTile {
+  using C = PfCfg<T, D>;
+  static constexpr int PPR = D / C::E;                         // data slots per row
+  static constexpr int KSLOT = C::KP * (int)sizeof(T) / 16;    // slots per K row
+  static constexpr int VSLOT = C::VP * (int)sizeof(T) / 16;    // slots per V row
+  static_assert(C::KP * sizeof(T) % 16 == 0 && C::VP * sizeof(T) % 16 == 0, "slot pitch");
+  static constexpr int KBYTES = PF_BK * KSLOT * 16;            // == KSLOT KiB
+  static constexpr int VBYTES = PF_BK * VSLOT * 16;
 };
 
 struct TileInfo {
@@ -119,34 +129,30 @@ struct TileInfo {
 
 constexpr int PF_ER = 4;  // ring of list entries: tile kt+2 is fetched while kt is computed
 
-template <typename T, int D>
-struct PfSmem {
-  using C = PfCfg<T, D>;
-  char k[C::NBUF][C::KBYTES];
-  char v[C::NBUF][C::VBYTES];
-  uint32_t ent[PF_ER][PF_BK];
-  TileInfo info[PF_ER];
-};
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
 // ---------------------------------------------------------------------------
 // main kernel
 // ---------------------------------------------------------------------------
-// Three waves per SIMD (at most 168 registers) measured faster than two
-// (more room for the register-hungry d=80 tiles) and than four.
 template <typename T, int D>
-__global__ __launch_bounds__(PF_THREADS) __attribute__((amdgpu_waves_per_eu(3))) void prefill_attn_kernel(
+__device__ __forceinline__ void prefill_attn_body(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v, T* __restrict__ o,
     int32_t H, int32_t L, int64_t qs, int64_t kvs, int64_t os, float c2,
     const int32_t* __restrict__ vu, int32_t L_meta, const uint32_t* __restrict__ list,
     const int32_t* __restrict__ count, int32_t n_qt, int32_t L_pad, int32_t n_work) {
   using C = PfCfg<T, D>;
+  using TL = PfTile<T, D>;
   constexpr bool BF = sizeof(T) == 2;
-  constexpr int PPR = C::PPR;
-  constexpr int NPIECE = PF_BK * PPR;                       // pieces per K (or V) tile
-  constexpr int PPT = (NPIECE + PF_THREADS - 1) / PF_THREADS;  // pieces per thread
   constexpr int NDB = C::DP / 32;                           // output d blocks
 
-  __shared__ PfSmem<T, D> sm;
+  // Separate objects per buffer: the compiler then knows that a
+  // direct-to-LDS load into one buffer does not feed reads of the other.
+  __shared__ __align__(1024) char kbuf0[TL::KBYTES];
+  __shared__ __align__(1024) char vbuf0[TL::VBYTES];
+  __shared__ __align__(1024) char kbuf1[C::NBUF == 2 ? TL::KBYTES : 1024];
+  __shared__ __align__(1024) char vbuf1[C::NBUF == 2 ? TL::VBYTES : 1024];
+  __shared__ uint32_t ent_ring[PF_ER][PF_BK];
+  __shared__ TileInfo info_ring[PF_ER];
 
   // XCD-aware work order: consecutive work items (same (sequence, head),
   // heaviest query block first) land on the same XCD and share its L2.
@@ -181,14 +187,15 @@ __global__ __launch_bounds__(PF_THREADS) __attribute__((amdgpu_waves_per_eu(3)))
   constexpr bool ONES_SUM = BF && (C::DP != D);
   if constexpr (C::DP != D) {
     for (int b = 0; b < C::NBUF; ++b) {
+      char* vbuf = b == 0 ? vbuf0 : vbuf1;
       if constexpr (BF) {
-        uint16_t* vs = reinterpret_cast<uint16_t*>(sm.v[b]);
+        uint16_t* vs = reinterpret_cast<uint16_t*>(vbuf);
         for (int i = tid; i < PF_BK * (C::DP - D); i += PF_THREADS) {
           const int c = D + i % (C::DP - D);
           vs[(i / (C::DP - D)) * C::VP + c] = (c == D) ? (uint16_t)0x3f80 : (uint16_t)0;
         }
       } else {
-        float* vs = reinterpret_cast<float*>(sm.v[b]);
+        float* vs = reinterpret_cast<float*>(vbuf);
         for (int i = tid; i < PF_BK * (C::DP - D); i += PF_THREADS)
           vs[(i / (C::DP - D)) * C::VP + D + i % (C::DP - D)] = 0.f;
       }
@@ -215,10 +222,9 @@ __global__ __launch_bounds__(PF_THREADS) __attribute__((amdgpu_waves_per_eu(3)))
     for (int i = 0; i < 16; ++i) oacc[db][i] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
 
-  // ---- staging: list entries run two tiles ahead through an LDS ring, so
-  // the key/value rows of tile kt+1 are addressed from LDS and their loads
-  // are in flight while tile kt is multiplied ----
-  u32x4 kreg[PPT], vreg[PPT];
+  // ---- staging: list entries run two tiles ahead through an LDS ring; the
+  // key/value rows of tile kt+1 go global -> LDS by direct loads addressed
+  // from the ring while tile kt is multiplied ----
   uint32_t ereg = PF_NONE;
   auto nvalid_of = [&](int kt) { return min(PF_BK, n_vis - kt * PF_BK); };
   auto load_entries = [&](int kt) {
@@ -228,7 +234,7 @@ __global__ __launch_bounds__(PF_THREADS) __attribute__((amdgpu_waves_per_eu(3)))
     const int slot = kt % PF_ER;
     if (tid < 64) {
       const int nvalid = nvalid_of(kt);
-      sm.ent[slot][tid] = ereg;
+      ent_ring[slot][tid] = ereg;
       int vr = (tid < nvalid) ? (int)(ereg >> 24) : 255;
 #pragma unroll
       for (int off = 1; off < 64; off <<= 1) vr = min(vr, __shfl_xor(vr, off, 64));
@@ -239,62 +245,41 @@ __global__ __launch_bounds__(PF_THREADS) __attribute__((amdgpu_waves_per_eu(3)))
         ti.jmax = jmax;
         ti.vrmin = vr;
         ti.nvalid = nvalid;
-        sm.info[slot] = ti;
+        info_ring[slot] = ti;
       }
     }
   };
-  auto load_rows = [&](int kt) {  // entries of tile kt are in the ring
+  // one matrix (K or V) of tile kt into `dst`: slot sl = r*NSLOT + sg holds
+  // elements [sg*E, sg*E+E) of row r; pad slots are not written (they keep
+  // their initial contents); a padding row re-reads column 0 (its score is
+  // masked, so any finite row will do)
+  auto dma_matrix = [&](int kt, const T* src, char* dst, auto nslot_c) {
+    constexpr int NSLOT = decltype(nslot_c)::value;
+    constexpr int BLOCKS = NSLOT;  // 64 slots (1 KiB) per block
     const int slot = kt % PF_ER;
     const int nvalid = nvalid_of(kt);
 #pragma unroll
-    for (int p = 0; p < PPT; ++p) {
-      const int piece = p * PF_THREADS + tid;
-      const int r = piece / PPR, sg = piece % PPR;
-      kreg[p] = u32x4{0, 0, 0, 0};
-      vreg[p] = u32x4{0, 0, 0, 0};
-      if (piece < NPIECE && r < nvalid) {
-        const int j = (int)(sm.ent[slot][r] & 0x00ffffffu);
-        kreg[p] = ld16(kb + (int64_t)j * D + sg * Piece<T>::E);
-        vreg[p] = ld16(vb + (int64_t)j * D + sg * Piece<T>::E);
+    for (int rnd = 0; rnd < (BLOCKS + 3) / 4; ++rnd) {
+      const int blk = rnd * 4 + wave;
+      if (blk < BLOCKS) {
+        const int sl = blk * 64 + lane;
+        const int r = sl / NSLOT, sg = sl % NSLOT;
+        if (sg < TL::PPR) {
+          const int j = r < nvalid ? (int)(ent_ring[slot][r] & 0x00ffffffu) : 0;
+          __builtin_amdgcn_global_load_lds(src + (int64_t)j * D + sg * C::E,
+                                           (lds_ptr_t)(dst + blk * 1024), 16, 0, 0);
+        }
       }
     }
   };
-  auto store_rows = [&](int buf) {
-#pragma unroll
-    for (int p = 0; p < PPT; ++p) {
-      const int piece = p * PF_THREADS + tid;
-      if (piece >= NPIECE) continue;
-      const int r = piece / PPR, sg = piece % PPR;
-      if constexpr (BF) {
-        *reinterpret_cast<u32x4*>(sm.k[buf] + (r * C::KP + sg * 8) * 2) = kreg[p];
-        *reinterpret_cast<u32x4*>(sm.v[buf] + (r * C::VP + sg * 8) * 2) = vreg[p];
-      } else {
-        float* ks = reinterpret_cast<float*>(sm.k[buf]) + r * C::KP + sg * 4;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) ks[e] = __uint_as_float(kreg[p][e]);
-        *reinterpret_cast<u32x4*>(sm.v[buf] + (r * C::VP + sg * 4) * 4) = vreg[p];
-      }
-    }
+  auto dma_rows = [&](int kt, char* kdst, char* vdst) {
+    dma_matrix(kt, kb, kdst, std::integral_constant<int, TL::KSLOT>{});
+    dma_matrix(kt, vb, vdst, std::integral_constant<int, TL::VSLOT>{});
   };
 
-  load_entries(0);
-  store_entries(0);
-  if (nt > 1) {
-    load_entries(1);
-    store_entries(1);
-  }
-  __syncthreads();
-  load_rows(0);
-  store_rows(0);
-  __syncthreads();
-
-  for (int kt = 0; kt < nt; ++kt) {
-    const int cur = kt % C::NBUF;
-    if (kt + 2 < nt) load_entries(kt + 2);
-    if (kt + 1 < nt) load_rows(kt + 1);
-
-    const TileInfo ti = sm.info[kt % PF_ER];
-    const uint32_t* tent = sm.ent[kt % PF_ER];
+  auto compute = [&](int kt, const char* kcur, const char* vcur) {
+    const TileInfo ti = info_ring[kt % PF_ER];
+    const uint32_t* tent = ent_ring[kt % PF_ER];
     if (wave_live && ti.jmin <= Iw + 31) {
       const bool full = ti.nvalid == PF_BK && ti.jmax <= Iw && ti.vrmin >= Iw + 31 - I;
       // ---- S^T = K Q^T for the two 32-key blocks ----
@@ -304,14 +289,14 @@ __global__ __launch_bounds__(PF_THREADS) __attribute__((amdgpu_waves_per_eu(3)))
 #pragma unroll
         for (int i = 0; i < 16; ++i) sacc[kb2][i] = 0.f;
         if constexpr (BF) {
-          const char* krow = sm.k[cur] + ((kb2 * 32 + l32) * C::KP + g * 8) * 2;
+          const char* krow = kcur + ((kb2 * 32 + l32) * C::KP + g * 8) * 2;
 #pragma unroll
           for (int kk = 0; kk < C::KSTEPS; ++kk) {
             const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(krow + kk * 32));
             sacc[kb2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[kk], sacc[kb2], 0, 0, 0);
           }
         } else {
-          const float* krow = reinterpret_cast<const float*>(sm.k[cur]) + (kb2 * 32 + l32) * C::KP + g;
+          const float* krow = reinterpret_cast<const float*>(kcur) + (kb2 * 32 + l32) * C::KP + g;
 #pragma unroll
           for (int kk = 0; kk < C::KSTEPS; ++kk)
             sacc[kb2] = __builtin_amdgcn_mfma_f32_32x32x2f32(krow[2 * kk], qreg[kk], sacc[kb2], 0, 0, 0);
@@ -374,7 +359,7 @@ __global__ __launch_bounds__(PF_THREADS) __attribute__((amdgpu_waves_per_eu(3)))
         // A operand V^T[d][keys]: within each group of 16 lanes, lane j points
         // at V[kbase + j/4][dbase + 4*(j%4)]; the transposing read hands lane
         // i the four keys kbase..kbase+3 of column dbase + i.
-        const uint16_t* vs = reinterpret_cast<const uint16_t*>(sm.v[cur]);
+        const uint16_t* vs = reinterpret_cast<const uint16_t*>(vcur);
         const int G = lane >> 4, j16 = lane & 15;
         const uint16_t* vsrc = vs + (4 * g + (j16 >> 2)) * C::VP + 16 * (G & 1) + 4 * (j16 & 3);
 #pragma unroll
@@ -389,7 +374,7 @@ __global__ __launch_bounds__(PF_THREADS) __attribute__((amdgpu_waves_per_eu(3)))
           }
         }
       } else {
-        const float* vs = reinterpret_cast<const float*>(sm.v[cur]);
+        const float* vs = reinterpret_cast<const float*>(vcur);
 #pragma unroll
         for (int db = 0; db < NDB; ++db)
 #pragma unroll
@@ -402,11 +387,44 @@ __global__ __launch_bounds__(PF_THREADS) __attribute__((amdgpu_waves_per_eu(3)))
             }
       }
     }
+  };
 
-    if constexpr (C::NBUF == 1) __syncthreads();
-    if (kt + 1 < nt) store_rows((kt + 1) % C::NBUF);
+  // one tile: rows of kt+1 start moving, kt is multiplied, everything is
+  // waited for, the ring advances
+  auto iteration = [&](int kt, const char* kc, const char* vc, char* kn, char* vn) {
+    if constexpr (C::NBUF == 2) {
+      if (kt + 1 < nt) dma_rows(kt + 1, kn, vn);
+    }
+    if (kt + 2 < nt) load_entries(kt + 2);
+    compute(kt, kc, vc);
+    if constexpr (C::NBUF == 1) {
+      __syncthreads();
+      if (kt + 1 < nt) dma_rows(kt + 1, kn, vn);
+    }
+    wait_vmem();
     if (kt + 2 < nt) store_entries(kt + 2);
     __syncthreads();
+  };
+
+  load_entries(0);
+  store_entries(0);
+  if (nt > 1) {
+    load_entries(1);
+    store_entries(1);
+  }
+  __syncthreads();
+  dma_rows(0, kbuf0, vbuf0);
+  wait_vmem();
+  __syncthreads();
+
+  for (int kt = 0; kt < nt; kt += 2) {
+    if constexpr (C::NBUF == 2) {
+      iteration(kt, kbuf0, vbuf0, kbuf1, vbuf1);
+      if (kt + 1 < nt) iteration(kt + 1, kbuf1, vbuf1, kbuf0, vbuf0);
+    } else {
+      iteration(kt, kbuf0, vbuf0, kbuf0, vbuf0);
+      if (kt + 1 < nt) iteration(kt + 1, kbuf0, vbuf0, kbuf0, vbuf0);
+    }
   }
 
   // ---- epilogue: normalise and write; a <CL> row copies its value row ----
@@ -452,6 +470,28 @@ __global__ __launch_bounds__(PF_THREADS) __attribute__((amdgpu_waves_per_eu(3)))
     }
 }
 
+// bf16 runs at three waves per SIMD (at most 168 registers), measured faster
+// than two and than four; the fp32 variant (small parity cases) is not capped.
+template <int D>
+__global__ __launch_bounds__(PF_THREADS) __attribute__((amdgpu_waves_per_eu(3))) void prefill_attn_kernel_bf16(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
+    uint16_t* __restrict__ o, int32_t H, int32_t L, int64_t qs, int64_t kvs, int64_t os, float c2,
+    const int32_t* __restrict__ vu, int32_t L_meta, const uint32_t* __restrict__ list,
+    const int32_t* __restrict__ count, int32_t n_qt, int32_t L_pad, int32_t n_work) {
+  prefill_attn_body<uint16_t, D>(q, k, v, o, H, L, qs, kvs, os, c2, vu, L_meta, list, count, n_qt,
+                                 L_pad, n_work);
+}
+
+template <int D>
+__global__ __launch_bounds__(PF_THREADS) void prefill_attn_kernel_f32(
+    const float* __restrict__ q, const float* __restrict__ k, const float* __restrict__ v,
+    float* __restrict__ o, int32_t H, int32_t L, int64_t qs, int64_t kvs, int64_t os, float c2,
+    const int32_t* __restrict__ vu, int32_t L_meta, const uint32_t* __restrict__ list,
+    const int32_t* __restrict__ count, int32_t n_qt, int32_t L_pad, int32_t n_work) {
+  prefill_attn_body<float, D>(q, k, v, o, H, L, qs, kvs, os, c2, vu, L_meta, list, count, n_qt,
+                              L_pad, n_work);
+}
+
 template <typename T, int D>
 static int launch_prefill(const void* q, const void* k, const void* v, void* o, int32_t b,
                           int32_t H, int32_t L, int64_t qs, int64_t kvs, int64_t os, float scale,
@@ -461,10 +501,16 @@ static int launch_prefill(const void* q, const void* k, const void* v, void* o, 
   int rc = hip_check(hipGetLastError(), "span_masked_prefill_attn: plan launch");
   if (rc) return rc;
   const int n_work = b * H * n_qt;
-  prefill_attn_kernel<T, D><<<n_work, PF_THREADS, 0, stream>>>(
-      static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
-      static_cast<T*>(o), H, L, qs, kvs, os, scale * PF_LOG2E, vu, L_meta, list, count, n_qt,
-      L_pad, n_work);
+  if constexpr (sizeof(T) == 2)
+    prefill_attn_kernel_bf16<D><<<n_work, PF_THREADS, 0, stream>>>(
+        static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
+        static_cast<T*>(o), H, L, qs, kvs, os, scale * PF_LOG2E, vu, L_meta, list, count, n_qt,
+        L_pad, n_work);
+  else
+    prefill_attn_kernel_f32<D><<<n_work, PF_THREADS, 0, stream>>>(
+        static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
+        static_cast<T*>(o), H, L, qs, kvs, os, scale * PF_LOG2E, vu, L_meta, list, count, n_qt,
+        L_pad, n_work);
   return hip_check(hipGetLastError(), "span_masked_prefill_attn: launch");
 }
 
