@@ -152,6 +152,7 @@ __device__ __forceinline__ void prefill_attn_body(
   __shared__ __align__(1024) char kbuf1[C::NBUF == 2 ? TL::KBYTES : 1024];
   __shared__ __align__(1024) char vbuf1[C::NBUF == 2 ? TL::VBYTES : 1024];
   __shared__ uint32_t ent_ring[PF_ER][PF_BK];
+  __shared__ int32_t row_ring[PF_ER][PF_BK];  // bare row index per entry
   __shared__ TileInfo info_ring[PF_ER];
 
   // XCD-aware work order: consecutive work items (same (sequence, head),
@@ -239,6 +240,9 @@ __device__ __forceinline__ void prefill_attn_body(
 #pragma unroll
       for (int off = 1; off < 64; off <<= 1) vr = min(vr, __shfl_xor(vr, off, 64));
       const int jmax = __shfl((int)(ereg & 0x00ffffffu), nvalid - 1, 64);
+      // a padding row of the tile repeats the last valid row (its score is
+      // masked, so any finite row will do)
+      row_ring[slot][tid] = tid < nvalid ? (int)(ereg & 0x00ffffffu) : jmax;
       if (tid == 0) {
         TileInfo ti;
         ti.jmin = (int)(ereg & 0x00ffffffu);
@@ -249,32 +253,37 @@ __device__ __forceinline__ void prefill_attn_body(
       }
     }
   };
-  // one matrix (K or V) of tile kt into `dst`: slot sl = r*NSLOT + sg holds
-  // elements [sg*E, sg*E+E) of row r; pad slots are not written (they keep
-  // their initial contents); a padding row re-reads column 0 (its score is
-  // masked, so any finite row will do)
-  auto dma_matrix = [&](int kt, const T* src, char* dst, auto nslot_c) {
-    constexpr int NSLOT = decltype(nslot_c)::value;
-    constexpr int BLOCKS = NSLOT;  // 64 slots (1 KiB) per block
-    const int slot = kt % PF_ER;
-    const int nvalid = nvalid_of(kt);
-#pragma unroll
-    for (int rnd = 0; rnd < (BLOCKS + 3) / 4; ++rnd) {
-      const int blk = rnd * 4 + wave;
-      if (blk < BLOCKS) {
-        const int sl = blk * 64 + lane;
-        const int r = sl / NSLOT, sg = sl % NSLOT;
-        if (sg < TL::PPR) {
-          const int j = r < nvalid ? (int)(ent_ring[slot][r] & 0x00ffffffu) : 0;
-          __builtin_amdgcn_global_load_lds(src + (int64_t)j * D + sg * C::E,
-                                           (lds_ptr_t)(dst + blk * 1024), 16, 0, 0);
-        }
-      }
-    }
-  };
+  // K and V of tile kt into kdst/vdst: slot sl = r*NSLOT + sg of a matrix
+  // holds elements [sg*E, sg*E+E) of row r; pad slots are not written (they
+  // keep their initial contents).  All row indices are read from the ring
+  // first, then the copies are issued.  The indices come from row_ring, which
+  // holds them bare: no masking of the packed entry happens on this path.
+  constexpr int KRND = (TL::KSLOT + 3) / 4, VRND = (TL::VSLOT + 3) / 4;
   auto dma_rows = [&](int kt, char* kdst, char* vdst) {
-    dma_matrix(kt, kb, kdst, std::integral_constant<int, TL::KSLOT>{});
-    dma_matrix(kt, vb, vdst, std::integral_constant<int, TL::VSLOT>{});
+    const int32_t* rows = row_ring[kt % PF_ER];
+    int kj[KRND], vj[VRND];
+#pragma unroll
+    for (int rnd = 0; rnd < KRND; ++rnd)
+      kj[rnd] = rows[min(((rnd * 4 + wave) * 64 + lane) / TL::KSLOT, PF_BK - 1)];
+#pragma unroll
+    for (int rnd = 0; rnd < VRND; ++rnd)
+      vj[rnd] = rows[min(((rnd * 4 + wave) * 64 + lane) / TL::VSLOT, PF_BK - 1)];
+#pragma unroll
+    for (int rnd = 0; rnd < KRND; ++rnd) {
+      const int blk = rnd * 4 + wave;
+      const int sg = (blk * 64 + lane) % TL::KSLOT;
+      if (blk < TL::KSLOT && sg < TL::PPR)
+        __builtin_amdgcn_global_load_lds(kb + (int64_t)kj[rnd] * D + sg * C::E,
+                                         (lds_ptr_t)(kdst + blk * 1024), 16, 0, 0);
+    }
+#pragma unroll
+    for (int rnd = 0; rnd < VRND; ++rnd) {
+      const int blk = rnd * 4 + wave;
+      const int sg = (blk * 64 + lane) % TL::VSLOT;
+      if (blk < TL::VSLOT && sg < TL::PPR)
+        __builtin_amdgcn_global_load_lds(vb + (int64_t)vj[rnd] * D + sg * C::E,
+                                         (lds_ptr_t)(vdst + blk * 1024), 16, 0, 0);
+    }
   };
 
   auto compute = [&](int kt, const char* kcur, const char* vcur) {
