@@ -24,25 +24,35 @@
 
 namespace sckv {
 
-// Tuning (measured on MI355X over the OPT-1.3B, 3B-RoPE and batch-256
-// streaming decode shapes): 1024-row chunks, 4 rows per lane group in flight
-// per trip, 256 threads, chunk-major dispatch order.
-constexpr int DEC_THREADS = 256;
-constexpr int DEC_CH = 1024;  // rows per chunk (one workgroup)
+// Launch shapes, measured on MI355X over three decode shapes: 2048 slices of
+// about 560 rows (d=64), 512 slices of about 2100 rows (d=80, rotary) and
+// 8192 slices of about 1200 rows (d=80, rotary).  A slice is one (sequence,
+// head) pair.
+//  * Fewer than DEC_SINGLE_MIN slices: each slice is cut into chunks of
+//    about DEC_CH rows, one 4-wave workgroup each, and a second kernel merges
+//    the chunk partials.
+//  * Otherwise one workgroup per slice writes the output itself (no second
+//    launch): 4 waves (bf16) or 512 threads (fp32) below DEC_NARROW_MIN
+//    slices, and from there on 2 waves (bf16) or 256 threads (fp32), which
+//    keeps more workgroups resident per CU.
+constexpr int DEC_CH = 1024;
+constexpr int DEC_SINGLE_MIN = 512;
+constexpr int DEC_NARROW_MIN = 1024;
+constexpr int DEC_THREADS = 256;  // fp32 split chunks
 constexpr float LOG2E = 1.4426950408889634f;
 
 struct RopeTab {
   double w[40];  // theta^(-2i/d), i < d/2
 };
 
-template <typename T, int D>
+template <typename T, int D, int THREADS>
 struct DecCfg {
   static constexpr int E = Piece<T>::E;           // elements per piece
   static constexpr int LPR = D / E;               // pieces per row
   static constexpr int GRP = LPR <= 8 ? 8 : (LPR <= 16 ? 16 : 32);
   static constexpr int RPW = 64 / GRP;            // rows per wave per step
   static constexpr int U = 4;                     // steps per trip (loads in flight per lane: 2U)
-  static constexpr int NG = (DEC_THREADS / 64) * RPW;  // lane groups per workgroup
+  static constexpr int NG = (THREADS / 64) * RPW;  // lane groups per workgroup
 };
 
 // rotated piece `seg` of a head vector x (global), rotate-half convention;
@@ -83,14 +93,53 @@ __device__ __forceinline__ int step_kind(const int32_t* cur_tok, const int32_t* 
   return 0;
 }
 
+// Writes the final output of a slice whose step is not an ordinary append
+// (kind 1: <CL>, the output is v_new; kind 2/3: failure, NaN and a status
+// bit).  `tid` runs over `nthr` threads.
+// A slice's rows split into n chunks of `rows` rows (the last one shorter)
+// of at most about `ch` rows each.  Chunk starts are multiples of 16 rows:
+// a wave then reads whole 128-byte lines (a bf16 row of 80 elements is 160
+// bytes, so only every fourth row starts on a line; a chunk that started
+// between would make every load of its wave span one line more).
+struct ChunkPlan {
+  int n, rows;
+};
+constexpr int DEC_ALIGN = 16;
+// rows and ch are positive ints, so every sum below fits in 32 unsigned bits
+__device__ __forceinline__ ChunkPlan chunk_plan(int rows, int ch) {
+  const uint32_t r = (uint32_t)rows, c = (uint32_t)ch;
+  const uint32_t n0 = (r + c - 1) / c;
+  const uint32_t per = (r + n0 - 1) / n0;
+  const uint32_t cr = (per + DEC_ALIGN - 1) / DEC_ALIGN * DEC_ALIGN;
+  ChunkPlan p;
+  p.rows = (int)cr;
+  p.n = (int)((r + cr - 1) / cr);  // <= n0
+  return p;
+}
+
 template <typename T, int D>
-__global__ __launch_bounds__(DEC_THREADS) void decode_chunk_kernel(
+__device__ __forceinline__ void write_special(int kind, const T* v_new, T* o, int32_t* status,
+                                              int bh, int H, int tid, int nthr) {
+  if (kind >= 2 && tid == 0 && (bh % H) == 0 && status)
+    atomicOr(status, kind == 2 ? SCKV_STATUS_TOKEN : SCKV_STATUS_CAP);
+  for (int i = tid; i < D; i += nthr) {
+    if (kind == 1) o[(int64_t)bh * D + i] = v_new[(int64_t)bh * D + i];
+    else if constexpr (sizeof(T) == 2) o[(int64_t)bh * D + i] = (T)0x7fc0;  // bf16 NaN
+    else o[(int64_t)bh * D + i] = NAN;
+  }
+}
+
+// FINAL: the workgroup covers the whole slice (one chunk of L_cap rows) and
+// writes the output itself; otherwise it writes a partial for the combine.
+template <typename T, int D, int THREADS, bool FINAL>
+__global__ __launch_bounds__(THREADS) void decode_chunk_kernel(
     const T* __restrict__ q, const T* __restrict__ k_new, const T* __restrict__ v_new,
     T* __restrict__ k_cache, T* __restrict__ v_cache, const int32_t* __restrict__ kv_len,
     const int32_t* __restrict__ cur_tok, const int32_t* __restrict__ vu,
     const int32_t* __restrict__ pos, int32_t L_meta, int32_t H, int32_t L_cap, float qscale,
-    int rotate, RopeTab tab, float* __restrict__ part, int32_t n_chunk_max, int32_t n_work) {
-  using C = DecCfg<T, D>;
+    int rotate, RopeTab tab, float* __restrict__ part, int32_t n_chunk_max, int32_t n_work,
+    int32_t ch, T* __restrict__ o, int32_t* __restrict__ status) {
+  using C = DecCfg<T, D, THREADS>;
   constexpr int E = C::E, LPR = C::LPR, GRP = C::GRP, RPW = C::RPW, U = C::U, NG = C::NG;
   // chunk-major order: every slice's first chunk is dispatched before any
   // slice's second chunk, so the workgroups that start past a slice's last
@@ -99,12 +148,17 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_chunk_kernel(
   const int chunk = blockIdx.x / n_bh;
   const int bh = blockIdx.x % n_bh;
   const int s = bh / H;
-  if (step_kind(cur_tok, vu, kv_len, s, L_meta, L_cap) != 0) return;  // combine handles it
+  const int kind = step_kind(cur_tok, vu, kv_len, s, L_meta, L_cap);
+  if (kind != 0) {  // the combine handles it, or this workgroup when FINAL
+    if constexpr (FINAL) write_special<T, D>(kind, v_new, o, status, bh, H, threadIdx.x, THREADS);
+    return;
+  }
   const int n = kv_len[s];
-  const int rows = n + 1;
-  const int r0 = chunk * DEC_CH;
-  if (r0 >= rows) return;
-  const int r1 = min(r0 + DEC_CH, rows);
+  const int rows = n + 1;  // cache rows and the new row
+  const ChunkPlan cp = chunk_plan(rows, ch);
+  if (chunk >= cp.n) return;
+  const int r0 = chunk * cp.rows;
+  const int r1 = min(r0 + cp.rows, rows);
   const int rc = min(r1, n);  // cache rows of this chunk: [r0, rc)
 
   const int tid = threadIdx.x;
@@ -116,7 +170,7 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_chunk_kernel(
 
   const T* kb = k_cache + (int64_t)bh * L_cap * D;
   const T* vb = v_cache + (int64_t)bh * L_cap * D;
-  constexpr int TRIP = (DEC_THREADS / 64) * U * RPW;  // rows per trip of the workgroup
+  constexpr int TRIP = (THREADS / 64) * U * RPW;  // rows per trip of the workgroup
   const int base0 = r0 + wave * U * RPW;
 
   // streamed rows: the 2U loads of one trip are issued together
@@ -226,7 +280,7 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_chunk_kernel(
     if (seg == 0) { sm[grp] = m; sl[grp] = l; }
   }
   __syncthreads();
-  float* out = part + ((int64_t)bh * n_chunk_max + chunk) * (D + 2);
+  __shared__ float res[D];
   if (tid < D) {
     float M = -INFINITY;
     for (int i = 0; i < NG; ++i) M = fmaxf(M, sm[i]);
@@ -237,79 +291,411 @@ __global__ __launch_bounds__(DEC_THREADS) void decode_chunk_kernel(
       Lsum += sl[i] * w;
       ov += sacc[i][tid] * w;
     }
-    out[2 + tid] = ov;
-    if (tid == 0) { out[0] = M; out[1] = Lsum; }
+    if constexpr (FINAL) {
+      res[tid] = ov / Lsum;
+    } else {
+      float* out = part + ((int64_t)bh * n_chunk_max + chunk) * (D + 2);
+      out[2 + tid] = ov;
+      if (tid == 0) { out[0] = M; out[1] = Lsum; }
+    }
+  }
+  if constexpr (FINAL) {
+    __syncthreads();
+    if (tid < D / E) {
+      float f[E];
+#pragma unroll
+      for (int e = 0; e < E; ++e) f[e] = res[tid * E + e];
+      st16(o + (int64_t)bh * D + tid * E, Piece<T>::pack(f));
+    }
   }
 }
 
+// One wave per slice: log-sum-exp merge of the slice's chunk partials, 64
+// chunks at a time (lane c holds chunk c's weight; the output elements are
+// spread over the lanes).
 template <typename T, int D>
-__global__ __launch_bounds__(128) void decode_combine_kernel(
+__global__ __launch_bounds__(64) void decode_combine_kernel(
     const T* __restrict__ v_new, const int32_t* __restrict__ kv_len,
     const int32_t* __restrict__ cur_tok, const int32_t* __restrict__ vu, int32_t L_meta,
-    int32_t H, int32_t L_cap, const float* __restrict__ part, int32_t n_chunk_max,
+    int32_t H, int32_t L_cap, const float* __restrict__ part, int32_t n_chunk_max, int32_t ch,
     T* __restrict__ o, int32_t* __restrict__ status) {
-  constexpr int E = Piece<T>::E;
   const int bh = blockIdx.x;
   const int s = bh / H;
-  const int tid = threadIdx.x;
+  const int lane = threadIdx.x;
   const int kind = step_kind(cur_tok, vu, kv_len, s, L_meta, L_cap);
-  if (kind >= 2 && tid == 0 && (bh % H) == 0 && status)
-    atomicOr(status, kind == 2 ? SCKV_STATUS_TOKEN : SCKV_STATUS_CAP);
-  __shared__ float res[D];
-  __shared__ float cw[128];  // chunk weights exp2(m_c - M), a block of 128 chunks at a time
-  __shared__ float red[2];
   if (kind != 0) {
-    if (tid < D) {
-      float r = NAN;
-      if (kind == 1) {
-        const T* vn = v_new + (int64_t)bh * D;
-        if constexpr (sizeof(T) == 2) r = bf16_lo((uint32_t)vn[tid]);
-        else r = vn[tid];
-      }
-      res[tid] = r;
-    }
-  } else {
-    const int nch = (kv_len[s] + 1 + DEC_CH - 1) / DEC_CH;
-    const float* p = part + (int64_t)bh * n_chunk_max * (D + 2);
-    // global max over the chunk maxima (one wave)
-    if (tid < 64) {
-      float M = -INFINITY;
-      for (int c = tid; c < nch; c += 64) M = fmaxf(M, p[c * (D + 2)]);
+    write_special<T, D>(kind, v_new, o, status, bh, H, lane, 64);
+    return;
+  }
+  const int nch = chunk_plan(kv_len[s] + 1, ch).n;
+  const float* p = part + (int64_t)bh * n_chunk_max * (D + 2);
+  constexpr int PER = (D + 63) / 64;  // output elements per lane
+  float M = -INFINITY, lsum = 0.f, acc[PER];
 #pragma unroll
-      for (int off = 32; off > 0; off >>= 1) M = fmaxf(M, __shfl_xor(M, off, 64));
-      if (tid == 0) red[0] = M;
+  for (int j = 0; j < PER; ++j) acc[j] = 0.f;
+  for (int c0 = 0; c0 < nch; c0 += 64) {
+    const int c = c0 + lane;
+    float mc = -INFINITY, lc = 0.f;
+    if (c < nch) {
+      mc = p[c * (D + 2)];
+      lc = p[c * (D + 2) + 1];
     }
-    __syncthreads();
-    const float M = red[0];
-    float Lsum = 0.f, acc = 0.f;
-    for (int c0 = 0; c0 < nch; c0 += 128) {
-      const int c = c0 + tid;
-      if (c < nch) {
-        const float mc = p[c * (D + 2)];
-        const float w = (mc == -INFINITY) ? 0.f : exp2f(mc - M);
-        cw[tid] = w;
-      }
-      __syncthreads();
-      const int cn = min(128, nch - c0);
-      if (tid < D) {
-#pragma unroll 8
-        for (int i = 0; i < cn; ++i) {
-          const float w = cw[i];
-          const float* pc = p + (c0 + i) * (D + 2);
-          Lsum = fmaf(pc[1], w, Lsum);
-          acc = fmaf(pc[2 + tid], w, acc);
-        }
-      }
-      __syncthreads();
+    float mb = mc;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) mb = fmaxf(mb, __shfl_xor(mb, off, 64));
+    const float mn = fmaxf(M, mb);    // finite: every chunk holds a row
+    const float sc = exp2f(M - mn);   // 0 on the first block (M = -inf)
+    lsum *= sc;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) acc[j] *= sc;
+    const float w = c < nch ? exp2f(mc - mn) : 0.f;
+    lsum = fmaf(lc, w, lsum);
+    const int cn = min(64, nch - c0);
+#pragma unroll 4
+    for (int i = 0; i < cn; ++i) {
+      const float wi = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, w), i));
+      const float* pc = p + (c0 + i) * (D + 2) + 2;
+#pragma unroll
+      for (int j = 0; j < PER; ++j)
+        if (lane + 64 * j < D) acc[j] = fmaf(pc[lane + 64 * j], wi, acc[j]);
     }
-    if (tid < D) res[tid] = acc / Lsum;
+    M = mn;
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) lsum += __shfl_xor(lsum, off, 64);
+  const float inv = 1.f / lsum;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const int e = lane + 64 * j;
+    if (e < D) {
+      if constexpr (sizeof(T) == 2) o[(int64_t)bh * D + e] = f32_to_bf16(acc[j] * inv);
+      else o[(int64_t)bh * D + e] = acc[j] * inv;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// bf16 caches: scores on the matrix cores
+// ---------------------------------------------------------------------------
+// A wave takes 32-row blocks of the chunk (block i of the chunk goes to wave
+// i mod NW).  Lane l owns key row l%32 of the block and elements
+// 16kk + 8(l/32) .. +7 (kk < D/16) of that row's key and value: exactly the
+// B operand of v_mfma_f32_32x32x16_bf16 for B[k][n] = K[n][k].  With the A
+// operand holding q in every one of its 32 rows, every column n of the
+// result is the score of key n, so each lane ends up with the score of its
+// own key and weighs its own value elements with it (no cross-lane traffic
+// per row).  q is split into two bf16 terms (hi + lo) so that the scores
+// keep about fp32 accuracy.  The running maximum is raised only when a block
+// maximum exceeds it by DM_RESCALE (log2 units), which keeps rescaling rare;
+// accumulated weights stay below 2^DM_RESCALE per row.  The next block's
+// rows are in flight while a block is computed.
+constexpr float DM_RESCALE = 8.f;
+
+template <int D>
+__device__ __forceinline__ float rot_elem(const uint16_t* x, int t, bool rotate, double ps,
+                                          const double* inv) {
+  const float xv = bf16_lo((uint32_t)x[t]);
+  if (!rotate) return xv;
+  constexpr int HD = D / 2;
+  const bool first = t < HD;
+  const float pv = bf16_lo((uint32_t)x[first ? t + HD : t - HD]);
+  const double two_pi = 6.283185307179586476925286766559;
+  const double inv_two_pi = 0.15915494309189533576888376337251;
+  double ang = ps * inv[first ? t : t - HD];
+  ang -= two_pi * rint(ang * inv_two_pi);
+  float sn, cs;
+  sincosf((float)ang, &sn, &cs);
+  return first ? xv * cs - pv * sn : xv * cs + pv * sn;
+}
+
+// Sums v[0..NV) over the 32 lanes of each half-wave.  While NV is even a
+// step halves the values a lane keeps (the lane whose MASK bit is set keeps
+// the upper half); odd counts finish with plain butterflies.  On return the
+// lane holds the sums of values [base, base + count).
+template <int NV, int MASK>
+__device__ __forceinline__ void half_wave_reduce(float* v, int lane, int& base) {
+  if constexpr (MASK > 0) {
+    if constexpr (NV % 2 == 0) {
+      constexpr int HV = NV / 2;
+      const bool up = (lane & MASK) != 0;
+#pragma unroll
+      for (int j = 0; j < HV; ++j) {
+        const float send = up ? v[j] : v[j + HV];
+        const float keep = up ? v[j + HV] : v[j];
+        v[j] = keep + __shfl_xor(send, MASK, 64);
+      }
+      if (up) base += HV;
+      half_wave_reduce<HV, MASK / 2>(v, lane, base);
+    } else {
+#pragma unroll
+      for (int j = 0; j < NV; ++j) v[j] += __shfl_xor(v[j], MASK, 64);
+      half_wave_reduce<NV, MASK / 2>(v, lane, base);
+    }
+  }
+}
+template <int NV, int MASK>
+constexpr int half_wave_count() {
+  if constexpr (MASK == 0) return NV;
+  else if constexpr (NV % 2 == 0) return half_wave_count<NV / 2, MASK / 2>();
+  else return half_wave_count<NV, MASK / 2>();
+}
+
+template <int D, int NW, bool FINAL>
+__global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_new,
+    const uint16_t* __restrict__ v_new, uint16_t* __restrict__ k_cache,
+    uint16_t* __restrict__ v_cache, const int32_t* __restrict__ kv_len,
+    const int32_t* __restrict__ cur_tok, const int32_t* __restrict__ vu,
+    const int32_t* __restrict__ pos, int32_t L_meta, int32_t H, int32_t L_cap, float qscale,
+    int rotate, RopeTab tab, float* __restrict__ part, int32_t n_chunk_max, int32_t n_work,
+    int32_t ch, uint16_t* __restrict__ o, int32_t* __restrict__ status) {
+  constexpr int KS = D / 16;     // k steps of 16 elements
+  constexpr int NA = 8 * KS;     // value elements per lane
+  constexpr int THREADS = NW * 64;
+  constexpr int HD = D / 2;
+  // chunk-major order (as in decode_chunk_kernel)
+  const int n_bh = n_work / n_chunk_max;
+  const int chunk = blockIdx.x / n_bh;
+  const int bh = blockIdx.x % n_bh;
+  const int s = bh / H;
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6;
+  const int lane = tid & 63;
+  const int kr = lane & 31;
+  const int h = lane >> 5;
+
+  // Everything the setup reads is wave-uniform and goes through scalar
+  // loads, whose counter is separate from that of the vector loads: the
+  // first two blocks of key/value rows are issued as soon as the slice
+  // length is known and arrive while q is prepared.  The block addresses use
+  // the length clamped into the cache, so they are valid whatever the step
+  // turns out to be.
+  const int n_raw = kv_len[s];
+  const int t_raw = cur_tok[s];
+  const uint32_t* qw = reinterpret_cast<const uint32_t*>(q + (int64_t)bh * D);
+  uint32_t qword[HD];
+#pragma unroll
+  for (int j = 0; j < HD; ++j) qword[j] = qw[j];
+  const bool t_ok = t_raw >= 0 && t_raw < L_meta;
+  const int vu_t = t_ok ? vu[(int64_t)s * L_meta + t_raw] : 0;
+  const int pos_t = (rotate && t_ok) ? pos[(int64_t)s * L_meta + t_raw] : 0;
+
+  const int n = min(max(n_raw, 0), L_cap - 1);
+  const int rows = n + 1;
+  const ChunkPlan cp = chunk_plan(rows, ch);
+  const int r0 = chunk * cp.rows;
+  const int r1 = min(r0 + cp.rows, rows);
+  const int rc = min(r1, n);  // cache rows of this chunk: [r0, rc)
+  const int nblk = chunk < cp.n ? (rc - r0 + 31) / 32 : 0;
+
+  const uint16_t* kb = k_cache + (int64_t)bh * L_cap * D;
+  const uint16_t* vb = v_cache + (int64_t)bh * L_cap * D;
+  // rows past rc re-read row rc-1 (always present when a block exists);
+  // their scores are masked
+  auto load_blk = [&](int i, u32x4* kd, u32x4* vd) {
+    const int row = min(r0 + 32 * i + kr, rc - 1);
+    const uint16_t* kp = kb + (int64_t)row * D + 8 * h;
+    const uint16_t* vp = vb + (int64_t)row * D + 8 * h;
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) kd[kk] = ld16(kp + 16 * kk);
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) vd[kk] = ld16(vp + 16 * kk);
+  };
+  u32x4 kA[KS], vA[KS], kB[KS], vB[KS];
+  if (wave < nblk) load_blk(wave, kA, vA);
+  if (wave + NW < nblk) load_blk(wave + NW, kB, vB);
+
+  // the step kind, with the precedence of step_kind()
+  const int kind = !t_ok ? 2 : (vu_t == t_raw ? 1 : ((n_raw < 0 || n_raw >= L_cap) ? 3 : 0));
+  if (kind != 0) {
+    if constexpr (FINAL) write_special<uint16_t, D>(kind, v_new, o, status, bh, H, tid, THREADS);
+    return;
+  }
+  if (chunk >= cp.n) return;
+
+  // rotated q element tid (tid < D) from the words held in scalar registers;
+  // the frequencies go to LDS for the new key
+  __shared__ float qs[D];
+  __shared__ double inv[HD];
+  if (tid < D) {
+    const int tp = tid < HD ? tid + HD : tid - HD;
+    uint32_t xw = 0, pw = 0;
+#pragma unroll
+    for (int j = 0; j < HD; ++j) {
+      xw = (tid >> 1) == j ? qword[j] : xw;
+      pw = (tp >> 1) == j ? qword[j] : pw;
+    }
+    float x = (tid & 1) ? bf16_hi(xw) : bf16_lo(xw);
+    if (rotate) {
+      const float pv = (tp & 1) ? bf16_hi(pw) : bf16_lo(pw);
+      double w = 0.0;
+#pragma unroll
+      for (int j = 0; j < HD; ++j) w = (tid % HD) == j ? tab.w[j] : w;
+      if (tid < HD) inv[tid] = w;
+      const double two_pi = 6.283185307179586476925286766559;
+      const double inv_two_pi = 0.15915494309189533576888376337251;
+      double ang = (double)pos_t * w;
+      ang -= two_pi * rint(ang * inv_two_pi);
+      float sn, cs;
+      sincosf((float)ang, &sn, &cs);
+      x = tid < HD ? x * cs - pv * sn : x * cs + pv * sn;
+    }
+    qs[tid] = x;
   }
   __syncthreads();
-  if (tid < D / E) {
-    float f[E];
+
+  bf16x8 qhi[KS], qlo[KS];
 #pragma unroll
-    for (int e = 0; e < E; ++e) f[e] = res[tid * E + e];
-    st16(o + (int64_t)bh * D + tid * E, Piece<T>::pack(f));
+  for (int kk = 0; kk < KS; ++kk) {
+    u32x4 wh, wl;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float x0 = qs[16 * kk + 8 * h + 2 * i], x1 = qs[16 * kk + 8 * h + 2 * i + 1];
+      const uint32_t hw = pack_bf16x2(x0, x1);
+      wh[i] = hw;
+      wl[i] = pack_bf16x2(x0 - bf16_lo(hw), x1 - bf16_hi(hw));
+    }
+    qhi[kk] = __builtin_bit_cast(bf16x8, wh);
+    qlo[kk] = __builtin_bit_cast(bf16x8, wl);
+  }
+
+  float M = -INFINITY, l = 0.f, acc[NA];
+#pragma unroll
+  for (int a = 0; a < NA; ++a) acc[a] = 0.f;
+  // takes a score (wave-uniform block maximum over lanes); returns its weight
+  auto weigh = [&](float sc) {
+    float mb = sc;
+#pragma unroll
+    for (int off = 16; off > 0; off >>= 1) mb = fmaxf(mb, __shfl_xor(mb, off, 64));
+    if (mb > M + DM_RESCALE) {
+      const float f = exp2f(M - mb);  // 0 while M = -inf
+      l *= f;
+#pragma unroll
+      for (int a = 0; a < NA; ++a) acc[a] *= f;
+      M = mb;
+    }
+    return exp2f(sc - M);
+  };
+  auto compute = [&](int i, const u32x4* kd, const u32x4* vd) {
+    f32x16 c;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) c[v] = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+      const bf16x8 kv = __builtin_bit_cast(bf16x8, kd[kk]);
+      c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qhi[kk], kv, c, 0, 0, 0);
+      c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qlo[kk], kv, c, 0, 0, 0);
+    }
+    const float sc = (r0 + 32 * i + kr < rc) ? c[0] * qscale : -INFINITY;
+    const float p = weigh(sc);
+    if (h == 0) l += p;
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t w = vd[kk][j];
+        acc[8 * kk + 2 * j] = fmaf(p, bf16_lo(w), acc[8 * kk + 2 * j]);
+        acc[8 * kk + 2 * j + 1] = fmaf(p, bf16_hi(w), acc[8 * kk + 2 * j + 1]);
+      }
+    }
+  };
+
+  // blocks wave, wave + NW are in flight; each computed buffer is refilled
+  // with the block 2 NW further on
+  for (int i = wave; i < nblk; i += 2 * NW) {
+    compute(i, kA, vA);
+    if (i + 2 * NW < nblk) load_blk(i + 2 * NW, kA, vA);
+    if (i + NW >= nblk) break;
+    compute(i + NW, kB, vB);
+    if (i + 3 * NW < nblk) load_blk(i + 3 * NW, kB, vB);
+  }
+
+  // the new row: rotated k_new (rounded to bf16 as stored) and v_new, taken
+  // in by wave 0 and written to the cache
+  if (n >= r0 && n < r1 && wave == 0) {
+    const uint16_t* kx = k_new + (int64_t)bh * D;
+    const uint16_t* vx = v_new + (int64_t)bh * D;
+    float prod = 0.f;
+    uint16_t kq[2] = {0, 0};
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int t = lane + 64 * u;
+      if (t < D) {
+        kq[u] = f32_to_bf16(rot_elem<D>(kx, t, rotate, (double)pos_t, inv));
+        prod = fmaf(qs[t], bf16_lo((uint32_t)kq[u]), prod);
+      }
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) prod += __shfl_xor(prod, off, 64);
+    // every lane takes the score; lanes 0 and 32 add the value elements they
+    // own, lane 0 counts the weight
+    const float p = weigh(prod * qscale);
+    if (lane == 0) l += p;
+    if (kr == 0) {
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) {
+        const u32x4 w = ld16(vx + 16 * kk + 8 * h);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          acc[8 * kk + 2 * j] = fmaf(p, bf16_lo(w[j]), acc[8 * kk + 2 * j]);
+          acc[8 * kk + 2 * j + 1] = fmaf(p, bf16_hi(w[j]), acc[8 * kk + 2 * j + 1]);
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int t = lane + 64 * u;
+      if (t < D) {
+        k_cache[((int64_t)bh * L_cap + n) * D + t] = kq[u];
+        v_cache[((int64_t)bh * L_cap + n) * D + t] = vx[t];
+      }
+    }
+  }
+
+  // wave partials: l over the wave, values over each half-wave
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) l += __shfl_xor(l, off, 64);
+  int base = 0;
+  half_wave_reduce<NA, 16>(acc, lane, base);
+  constexpr int NF = half_wave_count<NA, 16>();
+  __shared__ float sm[NW], sl[NW];
+  __shared__ float sacc[NW][D];
+#pragma unroll
+  for (int j = 0; j < NF; ++j) {
+    const int a = base + j;
+    sacc[wave][16 * (a / 8) + 8 * h + a % 8] = acc[j];
+  }
+  if (lane == 0) { sm[wave] = M; sl[wave] = l; }
+  __syncthreads();
+  __shared__ float res[D];
+  if (tid < D) {
+    float Mx = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) Mx = fmaxf(Mx, sm[w]);
+    float Ls = 0.f, ov = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      if (sm[w] == -INFINITY) continue;
+      const float f = exp2f(sm[w] - Mx);
+      Ls += sl[w] * f;
+      ov += sacc[w][tid] * f;
+    }
+    if constexpr (FINAL) {
+      res[tid] = ov / Ls;
+    } else {
+      float* out = part + ((int64_t)bh * n_chunk_max + chunk) * (D + 2);
+      out[2 + tid] = ov;
+      if (tid == 0) { out[0] = Mx; out[1] = Ls; }
+    }
+  }
+  if constexpr (FINAL) {
+    __syncthreads();
+    if (tid < D / 8) {
+      float f[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) f[e] = res[tid * 8 + e];
+      st16(o + (int64_t)bh * D + tid * 8, Piece<uint16_t>::pack(f));
+    }
   }
 }
 
@@ -326,18 +712,52 @@ static int launch_decode(const void* q, const void* k_new, const void* v_new, vo
   const int rotate = theta > 0.f ? 1 : 0;
   if (rotate)
     for (int i = 0; i < D / 2; ++i) tab.w[i] = std::pow((double)theta, -2.0 * i / D);
-  const int nc = n_chunks(L_cap);
   float* part = static_cast<float*>(ws);
-  const int n_work = b * H * nc;
-  decode_chunk_kernel<T, D><<<n_work, DEC_THREADS, 0, stream>>>(
-      static_cast<const T*>(q), static_cast<const T*>(k_new), static_cast<const T*>(v_new),
-      static_cast<T*>(k_cache), static_cast<T*>(v_cache), kv_len, cur_tok, vu, pos, L_meta, H,
-      L_cap, scale * LOG2E, rotate, tab, part, nc, n_work);
+  const T* qq = static_cast<const T*>(q);
+  const T* kn = static_cast<const T*>(k_new);
+  const T* vn = static_cast<const T*>(v_new);
+  T* kc = static_cast<T*>(k_cache);
+  T* vc = static_cast<T*>(v_cache);
+  T* out = static_cast<T*>(o);
+  const float qs = scale * LOG2E;
+  const int slices = b * H;
+  if (slices >= DEC_SINGLE_MIN) {
+    const bool narrow = slices >= DEC_NARROW_MIN;
+    if constexpr (sizeof(T) == 2) {
+      if (narrow)
+        decode_mfma_kernel<D, 2, true><<<slices, 128, 0, stream>>>(
+            qq, kn, vn, kc, vc, kv_len, cur_tok, vu, pos, L_meta, H, L_cap, qs, rotate, tab, part,
+            1, slices, L_cap, out, status);
+      else
+        decode_mfma_kernel<D, 4, true><<<slices, 256, 0, stream>>>(
+            qq, kn, vn, kc, vc, kv_len, cur_tok, vu, pos, L_meta, H, L_cap, qs, rotate, tab, part,
+            1, slices, L_cap, out, status);
+    } else {
+      if (narrow)
+        decode_chunk_kernel<T, D, 256, true><<<slices, 256, 0, stream>>>(
+            qq, kn, vn, kc, vc, kv_len, cur_tok, vu, pos, L_meta, H, L_cap, qs, rotate, tab, part,
+            1, slices, L_cap, out, status);
+      else
+        decode_chunk_kernel<T, D, 512, true><<<slices, 512, 0, stream>>>(
+            qq, kn, vn, kc, vc, kv_len, cur_tok, vu, pos, L_meta, H, L_cap, qs, rotate, tab, part,
+            1, slices, L_cap, out, status);
+    }
+    return hip_check(hipGetLastError(), "compacted_decode_attn: launch");
+  }
+  const int nc = n_chunks(L_cap);
+  const int n_work = slices * nc;
+  if constexpr (sizeof(T) == 2)
+    decode_mfma_kernel<D, 4, false><<<n_work, 256, 0, stream>>>(
+        qq, kn, vn, kc, vc, kv_len, cur_tok, vu, pos, L_meta, H, L_cap, qs, rotate, tab, part, nc,
+        n_work, DEC_CH, out, status);
+  else
+    decode_chunk_kernel<T, D, DEC_THREADS, false><<<n_work, DEC_THREADS, 0, stream>>>(
+        qq, kn, vn, kc, vc, kv_len, cur_tok, vu, pos, L_meta, H, L_cap, qs, rotate, tab, part, nc,
+        n_work, DEC_CH, out, status);
   int rc = hip_check(hipGetLastError(), "compacted_decode_attn: chunk launch");
   if (rc) return rc;
-  decode_combine_kernel<T, D><<<b * H, 128, 0, stream>>>(
-      static_cast<const T*>(v_new), kv_len, cur_tok, vu, L_meta, H, L_cap, part, nc,
-      static_cast<T*>(o), status);
+  decode_combine_kernel<T, D><<<slices, 64, 0, stream>>>(vn, kv_len, cur_tok, vu, L_meta, H, L_cap,
+                                                          part, nc, DEC_CH, out, status);
   return hip_check(hipGetLastError(), "compacted_decode_attn: combine launch");
 }
 

@@ -339,11 +339,16 @@ def test_compaction_incremental_equals_one_shot():
 # decode
 # ---------------------------------------------------------------------------
 
-@pytest.mark.parametrize("dtype,d,theta", [("bf16", 64, 0.0), ("bf16", 80, 10000.0),
-                                           ("f32", 64, 0.0), ("f32", 80, 10000.0)])
-def test_decode_matches_oracle(dtype, d, theta):
-    say(f"decode dtype={dtype} d={d} theta={theta}")
-    H, L_cap = 3, 700
+# The launch shape follows the number of (sequence, head) slices: H=3 gives
+# 24 slices, split into chunks merged by a second kernel; H=64 gives 512
+# slices and H=128 gives 1024, one workgroup each (wide, then narrow).
+@pytest.mark.parametrize("dtype,d,theta,H", [("bf16", 64, 0.0, 3), ("bf16", 80, 10000.0, 3),
+                                             ("f32", 64, 0.0, 3), ("f32", 80, 10000.0, 3),
+                                             ("bf16", 80, 10000.0, 64), ("f32", 64, 0.0, 64),
+                                             ("bf16", 64, 0.0, 128), ("f32", 80, 10000.0, 128)])
+def test_decode_matches_oracle(dtype, d, theta, H):
+    say(f"decode dtype={dtype} d={d} theta={theta} H={H}")
+    L_cap = 700
     lens = [0, 1, 255, 256, 257, 511, 600, 699]
     b = len(lens)
     spans = [[(650, 660)] for _ in range(b)]
@@ -386,16 +391,17 @@ def test_decode_matches_oracle(dtype, d, theta):
             assert torch.equal(cache.kv[:, :, s, :, :n], before[:, :, s, :, :n])
 
 
-def test_decode_reports_capacity_and_token_errors():
-    say("decode status")
-    H, L_cap, d = 2, 64, 64
+@pytest.mark.parametrize("dtype,H", [("bf16", 2), ("bf16", 256), ("bf16", 512), ("f32", 512)])
+def test_decode_reports_capacity_and_token_errors(dtype, H):
+    say(f"decode status dtype={dtype} H={H}")
+    L_cap, d = 64, 64
     meta = P().SpanMeta([[], []], 100, DEV)
-    cache = P().KVCache(1, 2, H, L_cap, d, torch.bfloat16, DEV)
+    cache = P().KVCache(1, 2, H, L_cap, d, W().torch_dtype(dtype), DEV)
     cache.kv.zero_()
     cache.kv_len.copy_(torch.tensor([L_cap, 3], dtype=torch.int32))
     cache.cur_tok.copy_(torch.tensor([10, 100], dtype=torch.int32))
     ws = P().Workspace(2, H, 1, L_cap, d, DEV)
-    q = rnd((2, H, d), 1, "bf16")
+    q = rnd((2, H, d), 1, dtype)
     o = torch.zeros_like(q)
     P().decode_layer(q, q, q, cache, 0, meta, ws, o)
     torch.cuda.synchronize()
