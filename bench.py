@@ -351,13 +351,16 @@ def main():
         if rec is not None:
             rec["t2"].record()
         for t in range(steps):
+            # one event pair around the M back-to-back decode calls of a step:
+            # a pair around every call would add the events' own overhead to
+            # each call
+            if rec is not None and use_ev:
+                rec["dec"][t][0].record()
             for m in range(M):
-                if rec is not None and use_ev:
-                    rec["dec"][t * M + m][0].record()
                 P.decode_layer(q_dec[t, m], k_dec[t, m], v_dec[t, m], cache, m, meta, ws, od,
                                theta=theta)
-                if rec is not None and use_ev:
-                    rec["dec"][t * M + m][1].record()
+            if rec is not None and use_ev:
+                rec["dec"][t][1].record()
             cache.commit(meta)
         if rec is not None:
             rec["t3"].record()
@@ -369,7 +372,7 @@ def main():
     for _ in range(args.steps):
         recs.append({"t0": E(), "t1": E(), "t2": E(), "t3": E(),
                      "pf": [(E(), E()) for _ in range(M)] if use_ev else None,
-                     "dec": [(E(), E()) for _ in range(n_dec)] if use_ev else None})
+                     "dec": [(E(), E()) for _ in range(steps)] if use_ev else None})
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     for r in recs:
@@ -401,11 +404,11 @@ def main():
     cmp_ms = [r["t1"].elapsed_time(r["t2"]) for r in recs]
     decph_ms = [r["t2"].elapsed_time(r["t3"]) for r in recs]
     if use_ev:
-        dec_launch_ms = np.array([[a.elapsed_time(z) for a, z in r["dec"]] for r in recs])
+        dec_step_ms = np.array([[a.elapsed_time(z) for a, z in r["dec"]] for r in recs])
         pf_launch_ms = np.array([[a.elapsed_time(z) for a, z in r["pf"]] for r in recs])
-        dec_avg_ms = float(dec_launch_ms.mean())
+        dec_total_ms = float(dec_step_ms.sum(axis=1).mean())
+        dec_avg_ms = dec_total_ms / n_dec
         pf_avg_ms = float(pf_launch_ms.mean())
-        dec_total_ms = float(dec_launch_ms.sum(axis=1).mean())
     else:
         dec_avg_ms = float(np.mean(decph_ms)) / n_dec
         pf_avg_ms = float(np.mean(pre_ms)) / M
@@ -416,6 +419,14 @@ def main():
     pf_tflops_alg = pf_alg / (pf_avg_ms * 1e-3) / 1e12
     ms_per_step = float(np.mean(step_ms))
 
+    # the library's launch shape: one workgroup per (sequence, head) slice from
+    # 512 slices on, chunks plus a merge kernel below
+    if b * H >= 512:
+        dec_kernel = "decode_mfma_kernel"
+        dec_launch = "one compacted_decode_attn call = one kernel, one workgroup per (sequence, head)"
+    else:
+        dec_kernel = "decode_mfma_kernel + decode_combine_kernel"
+        dec_launch = "one compacted_decode_attn call = chunk kernel + combine kernel"
     wl_key = f"{w.name}/steps{steps}"
     dec_traffic = stored_traffic("traffic_decode_3b-rope.json", wl_key)
     pf_traffic = stored_traffic("traffic_prefill_3b-rope.json", wl_key)
@@ -437,7 +448,7 @@ def main():
                    "heads": H, "d_head": d, "seq_len": L, "evicted": 0.5,
                    "decode_steps": steps, "rope_theta": theta, "L_cap": L_cap,
                    "parallelism": "single-gpu"},
-        "roofline": {"bound": "hbm", "kernel": "decode_chunk_kernel (compacted_decode_attn)",
+        "roofline": {"bound": "hbm", "kernel": dec_kernel + " (compacted_decode_attn)",
                      "achieved": round(dec_bytes_launch / (dec_avg_ms * 1e-3) / 1e9, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(dec_bytes_launch / (dec_avg_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
@@ -446,7 +457,7 @@ def main():
                      else round(dec_traffic / dec_bytes_launch, 4),
                      "avg_launch_us": round(dec_avg_ms * 1e3, 2),
                      "bytes_per_launch": int(dec_bytes_launch),
-                     "launch": "one compacted_decode_attn call = chunk kernel + combine kernel"},
+                     "launch": dec_launch},
         "roofline_prefill": {"bound": "mfma", "kernel": "prefill_attn_kernel (span_masked_prefill_attn)",
                              "achieved": round(pf_tflops_exe, 1), "peak": BF16_PEAK_TFLOPS,
                              "unit": "TFLOP/s", "frac": round(pf_tflops_exe / BF16_PEAK_TFLOPS, 4),

@@ -192,8 +192,12 @@ int kv_compact(void* kv, void* kv_out, int32_t M, int32_t b, int32_t H, int32_t 
  *          holding the split-K partials (overwritten; calls that share a
  *          workspace must be ordered, e.g. enqueued on one stream).
  * status : nullable int32, status bits OR-ed in.
- * The key rows are split into chunks of 1024 rows, one workgroup each; a
- * second kernel merges the chunk partials (log-sum-exp) into o.
+ * Launch shape: with b*H >= 512 one workgroup per (sequence, head) covers
+ * all its rows and writes o (the workspace is not touched); with fewer, the
+ * rows are cut into balanced chunks of at most about 1024 rows, one
+ * workgroup each, and a second kernel merges the chunk partials
+ * (log-sum-exp) into o.  bf16 scores are computed on the matrix cores with
+ * q carried as two bf16 terms (about fp32 accuracy).
  * ------------------------------------------------------------------------- */
 size_t sckv_decode_workspace_bytes(int32_t b, int32_t H, int32_t L_cap, int32_t d_head);
 int compacted_decode_attn(const void* q, const void* k_new, const void* v_new, void* k_cache,
