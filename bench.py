@@ -49,6 +49,11 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--gen-tokens", type=int, default=None,
                     help="streaming workload: generated tokens per run (default: all)")
+    ap.add_argument("--span-sweep", action="store_true",
+                    help="span lengths U(2,25) at each of --sweep-ratios instead of the "
+                         "workload's own spans")
+    ap.add_argument("--sweep-ratios", type=float, nargs="+",
+                    default=[0.1, 0.3, 0.5, 0.7, 0.9])
     return ap.parse_args()
 
 
@@ -328,14 +333,25 @@ def main():
 
     import torch
 
-    from paper_2310_08152_amd import path as P
     from paper_2310_08152_amd import workload as W
 
-    dev = "cuda:0"
     torch.cuda.set_device(0)
     w = W.get_workload(args.workload)
     if w.gen_tokens > 0:
         return run_streaming(args, w)
+    if args.span_sweep:
+        return run_span_sweep(args, w)
+    print(json.dumps(measure(args, w)), flush=True)
+
+
+def measure(args, w):
+    """One bench line for a prefill (+ compaction + decode) workload."""
+    import torch
+
+    from paper_2310_08152_amd import path as P
+    from paper_2310_08152_amd import workload as W
+
+    dev = "cuda:0"
     steps = w.decode_steps if args.decode_steps is None else args.decode_steps
     M, b, H, d, L = w.layers, w.batch, w.heads, w.d_head, w.seq_len
     theta = w.rope_theta
@@ -531,7 +547,57 @@ def main():
     elif not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, spans_all, k_in, v_in, q_dec, k_dec, v_dec,
                                            args.cpu_seconds)
-    print(json.dumps(out), flush=True)
+    elt = 2 if w.dtype == "bf16" else 4
+    live = int(n_keep.max()) + steps  # rows held by the longest sequence at the last step
+    out["kv_rows_decode_max"] = live
+    out["kv_bytes_decode"] = int(M * 2 * b * H * live * d * elt)
+    out["kv_bytes_allocated"] = int(M * 2 * b * H * L_cap * d * elt)
+    out["decode_tokens_per_s"] = (round(b * steps / (float(np.mean(decph_ms)) * 1e-3), 1)
+                                  if steps else None)
+    return out
+
+
+def run_span_sweep(args, w):
+    """The paper's span distribution (lengths uniform in [2, 25]) at a range
+    of compression ratios on the workload's shape: prefill, compaction and
+    decode throughput and the cache held during decode, per ratio."""
+    import dataclasses
+
+    import torch
+
+    points = []
+    for r in args.sweep_ratios:
+        wr = dataclasses.replace(w, name=f"{w.name} U(2,25) r={r}",
+                                 span_kind="uniform", span_args=dict(ratio=r, lo=2, hi=25))
+        out = measure(args, wr)
+        pt = {"ratio": r, "evicted": out["config"]["evicted"],
+              "prefill_tflops_executed": out["roofline_prefill"]["achieved"],
+              "prefill_tflops_algorithmic": out["roofline_prefill"]["algorithmic_tflops"],
+              "prefill_executed_over_algorithmic": out["roofline_prefill"]["executed_over_algorithmic"],
+              "prefill_ms_per_layer": round(out["roofline_prefill"]["avg_launch_us"] / 1e3, 4),
+              "compaction_gbs": out["compaction_gbs"],
+              "compaction_ms": out["phases_ms"]["compaction"],
+              "decode_gbs": out["value"], "decode_frac_of_hbm": out["roofline"]["frac"],
+              "decode_us_per_call": out["roofline"]["avg_launch_us"],
+              "decode_tokens_per_s": out["decode_tokens_per_s"],
+              "kv_rows_decode_max": out["kv_rows_decode_max"],
+              "kv_bytes_decode": out["kv_bytes_decode"],
+              "kv_bytes_allocated": out["kv_bytes_allocated"]}
+        points.append(pt)
+        print(json.dumps(pt), file=sys.stderr, flush=True)
+        torch.cuda.empty_cache()
+    M, b, H, d, L = w.layers, w.batch, w.heads, w.d_head, w.seq_len
+    steps = w.decode_steps if args.decode_steps is None else args.decode_steps
+    line = {"metric": "span-length U(2,25) sweep over compression ratio: prefill TFLOP/s, "
+                      "compaction GB/s, decode GB/s and tokens/s, decode-time KV bytes",
+            "value": None, "unit": None, "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "higher_is_better": True, "vs_baseline": None,
+            "dtype": w.dtype, "data": "synthetic",
+            "config": {"workload": f"{w.name} shape, spans U(2,25) at each ratio",
+                       "layers": M, "batch": b, "heads": H, "d_head": d, "seq_len": L,
+                       "decode_steps": steps, "rope_theta": w.rope_theta},
+            "sweep": points}
+    print(json.dumps(line), flush=True)
 
 
 if __name__ == "__main__":
