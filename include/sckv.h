@@ -122,6 +122,21 @@ int rope_apply(const void* x, void* y, int32_t b, int32_t H, int32_t n, int64_t 
                int32_t L_meta, int32_t tok0, float theta, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
+ * rope_apply into a cache at a per-sequence row: row t of x (token tok0 + t)
+ * goes to row row0[s] + t of y.  Used to append a block of the prompt to the
+ * compacted cache (Section 3, "Manipulating Key-Value Memory": a long prompt
+ * is processed block by block and freed progressively).
+ * row0   : [b] device; typically the output of kv_extend.
+ * y_rows : rows of each y slice (L_cap); y_stride_bh >= y_rows * d_head.
+ * A sequence with row0 < 0 or row0 + n > y_rows is not written and sets
+ * SCKV_STATUS_CAP in status (nullable).
+ * ------------------------------------------------------------------------- */
+int rope_apply_at(const void* x, void* y, const int32_t* row0, int32_t y_rows, int32_t b,
+                  int32_t H, int32_t n, int64_t x_stride_bh, int64_t y_stride_bh, int32_t d_head,
+                  sckv_dtype dt, const int32_t* pos, int32_t L_meta, int32_t tok0, float theta,
+                  int32_t* status, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
  * Causal attention under the <CL>/<CR> span-exclusion mask (prefill).
  * Paper: Section 1 (tokens after <CR> do not see the enclosed tokens) and
  * Section 3.1 (<CL> sees only itself; normal tokens see earlier <CR> and
@@ -135,7 +150,7 @@ int rope_apply(const void* x, void* y, int32_t b, int32_t H, int32_t n, int64_t 
  * vu    : [b][L_meta] span metadata from sckv_span_meta, L <= L_meta.
  * ws    : device workspace of at least sckv_prefill_workspace_bytes(b, L)
  *         bytes (overwritten).
- * Limits: 1 <= L <= 65536.  Key columns that no row of a query block may see
+ * Limits: 1 <= L <= 32768.  Key columns that no row of a query block may see
  * are never read.
  * ------------------------------------------------------------------------- */
 size_t sckv_prefill_workspace_bytes(int32_t b, int32_t L);
@@ -144,6 +159,37 @@ int span_masked_prefill_attn(const void* q, const void* k, const void* v, void* 
                              int64_t kv_stride_bh, int64_t o_stride_bh, sckv_dtype dt,
                              float scale, const int32_t* vu, int32_t L_meta, void* ws,
                              size_t ws_bytes, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
+ * The same masked attention for one block of the prompt whose keys and
+ * values are in a (compacted) cache: block-wise processing of a prompt that
+ * does not fit, freeing closed spans after each block (Section 3,
+ * "Manipulating Key-Value Memory for Inference-time Compression").
+ *
+ * q, o     : (b, H, nq, d_head): the block's queries, tokens tok0 .. tok0+nq-1.
+ * k_cache, v_cache : (b, H, L_cap, d_head) layer slices, slice stride
+ *            kv_stride_bh >= L_cap * d_head.  Row r of sequence s holds token
+ *            tok_idx[s][r]; rows [0, row0[s]) are earlier blocks' surviving
+ *            rows (ascending tokens, all < tok0) and rows row0[s] + i hold
+ *            token tok0 + i (written by rope_apply_at; tok_idx by kv_extend).
+ * row0     : [b] device; a sequence with row0 < 0 or row0 + nq > L_cap gets
+ *            NaN outputs, nothing is read, and SCKV_STATUS_CAP is set in
+ *            status (nullable).
+ * Output row i equals row tok0 + i of span_masked_prefill_attn over the
+ * whole prompt whenever the cache holds every row that row may see (which
+ * kv_compact at the block boundaries guarantees).
+ * ws       : >= sckv_prefill_cached_workspace_bytes(b, nq, L_cap) bytes.
+ * Limits: nq <= L_cap <= 32768; L_meta < 2^24 - 1.
+ * ------------------------------------------------------------------------- */
+size_t sckv_prefill_cached_workspace_bytes(int32_t b, int32_t nq, int32_t L_cap);
+int span_masked_prefill_attn_cached(const void* q, const void* k_cache, const void* v_cache,
+                                    void* o, int32_t b, int32_t H, int32_t nq, int32_t d_head,
+                                    int64_t q_stride_bh, int64_t kv_stride_bh,
+                                    int64_t o_stride_bh, sckv_dtype dt, float scale,
+                                    const int32_t* vu, int32_t L_meta, int32_t tok0,
+                                    const int32_t* row0, const int32_t* tok_idx, int32_t L_cap,
+                                    void* ws, size_t ws_bytes, int32_t* status,
+                                    hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
  * Free the key/value rows of closed spans, in place, keeping the survivors in
@@ -216,6 +262,19 @@ int compacted_decode_attn(const void* q, const void* k_new, const void* v_new, v
  * Paper: Section 3, "Manipulating Key-Value Memory" (the cache holds only rows
  * later tokens may see) with the position tie of "Input Transformation".
  * ------------------------------------------------------------------------- */
+/* ---------------------------------------------------------------------------
+ * Append bookkeeping for a block of n prompt tokens tok0 .. tok0+n-1 (all of
+ * them, sentinels included; kv_compact frees what the block closes): for
+ * each sequence, row0_out[s] = kv_len[s], rows kv_len[s] + i get
+ * tok_idx = tok0 + i and pos_ids = pos[s][tok0 + i], and kv_len[s] += n.
+ * A sequence without room (kv_len + n > L_cap) is left unchanged, gets
+ * row0_out[s] = -1 and sets SCKV_STATUS_CAP in status (nullable).
+ * Paper: Section 3, "Manipulating Key-Value Memory" (progressive freeing).
+ * ------------------------------------------------------------------------- */
+int kv_extend(int32_t* kv_len, int32_t* tok_idx, int32_t* pos_ids, int32_t* row0_out,
+              const int32_t* pos, int32_t L_meta, int32_t tok0, int32_t n, int32_t b,
+              int32_t L_cap, int32_t* status, hipStream_t stream);
+
 int kv_commit(int32_t* kv_len, int32_t* tok_idx, int32_t* pos_ids, int32_t* cur_tok,
               const int32_t* vu, const int32_t* pos, int32_t L_meta, int32_t b, int32_t L_cap,
               int32_t* status, hipStream_t stream);

@@ -50,7 +50,15 @@ _SIGS = {
     "sckv_span_meta": (ctypes.c_int, [_p, _p, _p, _i32, _i32, _i32, _p, _p, _p, _p]),
     "rope_apply": (ctypes.c_int, [_p, _p, _i32, _i32, _i32, _i64, _i64, _i32, ctypes.c_int, _p,
                                   _i32, _i32, _f32, _p]),
+    "rope_apply_at": (ctypes.c_int, [_p, _p, _p, _i32, _i32, _i32, _i32, _i64, _i64, _i32,
+                                     ctypes.c_int, _p, _i32, _i32, _f32, _p, _p]),
     "sckv_prefill_workspace_bytes": (_sz, [_i32, _i32]),
+    "sckv_prefill_cached_workspace_bytes": (_sz, [_i32, _i32, _i32]),
+    "span_masked_prefill_attn_cached": (ctypes.c_int, [_p, _p, _p, _p, _i32, _i32, _i32, _i32,
+                                                       _i64, _i64, _i64, ctypes.c_int, _f32, _p,
+                                                       _i32, _i32, _p, _p, _i32, _p, _sz, _p,
+                                                       _p]),
+    "kv_extend": (ctypes.c_int, [_p, _p, _p, _p, _p, _i32, _i32, _i32, _i32, _i32, _p, _p]),
     "span_masked_prefill_attn": (ctypes.c_int, [_p, _p, _p, _p, _i32, _i32, _i32, _i32, _i64,
                                                 _i64, _i64, ctypes.c_int, _f32, _p, _i32, _p, _sz,
                                                 _p]),
@@ -133,6 +141,35 @@ def rope_apply(x, y, b: int, H: int, n: int, x_stride_bh: int, y_stride_bh: int,
                pos, L_meta: int, tok0: int, theta: float, stream=None):
     _check(lib.rope_apply(_ptr(x), _ptr(y), b, H, n, x_stride_bh, y_stride_bh, d_head,
                           _dtype_code(x), _ptr(pos), L_meta, tok0, theta, _stream(stream, x)))
+
+
+def rope_apply_at(x, y, row0, y_rows: int, b: int, H: int, n: int, x_stride_bh: int,
+                  y_stride_bh: int, d_head: int, pos, L_meta: int, tok0: int, theta: float,
+                  status=None, stream=None):
+    _check(lib.rope_apply_at(_ptr(x), _ptr(y), _ptr(row0), y_rows, b, H, n, x_stride_bh,
+                             y_stride_bh, d_head, _dtype_code(x), _ptr(pos), L_meta, tok0, theta,
+                             _ptr(status), _stream(stream, x)))
+
+
+def sckv_prefill_cached_workspace_bytes(b: int, nq: int, L_cap: int) -> int:
+    return int(lib.sckv_prefill_cached_workspace_bytes(b, nq, L_cap))
+
+
+def span_masked_prefill_attn_cached(q, k_cache, v_cache, o, b: int, H: int, nq: int, d_head: int,
+                                    q_stride_bh: int, kv_stride_bh: int, o_stride_bh: int,
+                                    scale: float, vu, L_meta: int, tok0: int, row0, tok_idx,
+                                    L_cap: int, ws, status=None, stream=None):
+    _check(lib.span_masked_prefill_attn_cached(
+        _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(o), b, H, nq, d_head, q_stride_bh,
+        kv_stride_bh, o_stride_bh, _dtype_code(q), scale, _ptr(vu), L_meta, tok0, _ptr(row0),
+        _ptr(tok_idx), L_cap, _ptr(ws), ws.numel() * ws.element_size(), _ptr(status),
+        _stream(stream, q)))
+
+
+def kv_extend(kv_len, tok_idx, pos_ids, row0_out, pos, L_meta: int, tok0: int, n: int, b: int,
+              L_cap: int, status=None, stream=None):
+    _check(lib.kv_extend(_ptr(kv_len), _ptr(tok_idx), _ptr(pos_ids), _ptr(row0_out), _ptr(pos),
+                         L_meta, tok0, n, b, L_cap, _ptr(status), _stream(stream, kv_len)))
 
 
 def sckv_prefill_workspace_bytes(b: int, L: int) -> int:

@@ -81,12 +81,16 @@ struct InvFreq {
   double w[64];
 };
 
+// row0 (nullable): per sequence, the row of y that receives row 0 of x; a
+// sequence whose rows would leave [0, y_rows) (row0 < 0 included) is not
+// written and sets SCKV_STATUS_CAP.
 template <typename T, int D>
 __global__ __launch_bounds__(256) void rope_kernel(const T* x, T* y,
                                                    int32_t H, int32_t n, int64_t xs, int64_t ys,
                                                    const int32_t* __restrict__ pos, int32_t L_meta,
                                                    int32_t tok0, int64_t total, InvFreq inv,
-                                                   int rotate) {
+                                                   int rotate, const int32_t* __restrict__ row0,
+                                                   int32_t y_rows, int32_t* status) {
   constexpr int E = Piece<T>::E;
   constexpr int HALF = D / 2;
   constexpr int PPH = HALF / E;  // pieces per half row
@@ -99,8 +103,17 @@ __global__ __launch_bounds__(256) void rope_kernel(const T* x, T* y,
     const int t = (int)(rowg % n);
     const int64_t bh = rowg / n;
     const int s = (int)(bh / H);
+    int64_t drow = t;
+    if (row0) {
+      const int r0 = row0[s];
+      if (r0 < 0 || (int64_t)r0 + n > y_rows) {
+        if (status && t == 0 && p == 0) atomicOr(status, SCKV_STATUS_CAP);
+        continue;
+      }
+      drow += r0;
+    }
     const T* src = x + bh * xs + (int64_t)t * D;
-    T* dst = y + bh * ys + (int64_t)t * D;
+    T* dst = y + bh * ys + drow * D;
     u32x4 a = ld16(src + p * E), c = ld16(src + HALF + p * E);
     if (rotate) {
       float fa[E], fc[E];
@@ -150,6 +163,33 @@ __global__ void commit_kernel(int32_t* __restrict__ kv_len, int32_t* __restrict_
   cur_tok[s] = t + 1;
 }
 
+// ---------------------------------------------------------------------------
+// block append bookkeeping: one workgroup per sequence
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void extend_kernel(int32_t* __restrict__ kv_len,
+                                                     int32_t* __restrict__ tok_idx,
+                                                     int32_t* __restrict__ pos_ids,
+                                                     int32_t* __restrict__ row0_out,
+                                                     const int32_t* __restrict__ pos,
+                                                     int32_t L_meta, int32_t tok0, int32_t n,
+                                                     int32_t L_cap, int32_t* status) {
+  const int s = blockIdx.x;
+  const int r0 = kv_len[s];
+  const bool ok = r0 >= 0 && (int64_t)r0 + n <= L_cap;
+  if (ok) {
+    for (int i = threadIdx.x; i < n; i += blockDim.x) {
+      tok_idx[(int64_t)s * L_cap + r0 + i] = tok0 + i;
+      pos_ids[(int64_t)s * L_cap + r0 + i] = pos[(int64_t)s * L_meta + tok0 + i];
+    }
+  }
+  __syncthreads();  // every thread has read kv_len[s]
+  if (threadIdx.x == 0) {
+    row0_out[s] = ok ? r0 : -1;
+    if (ok) kv_len[s] = r0 + n;
+    else if (status) atomicOr(status, SCKV_STATUS_CAP);
+  }
+}
+
 }  // namespace sckv
 
 using namespace sckv;
@@ -195,6 +235,7 @@ extern "C" int sckv_span_meta(const int32_t* cl_host, const int32_t* cr_host,
 template <typename T, int D>
 static int launch_rope(const void* x, void* y, int32_t b, int32_t H, int32_t n, int64_t xs,
                        int64_t ys, const int32_t* pos, int32_t L_meta, int32_t tok0, float theta,
+                       const int32_t* row0, int32_t y_rows, int32_t* status,
                        hipStream_t stream) {
   InvFreq inv;
   for (int i = 0; i < 64; ++i) inv.w[i] = 0.0;
@@ -205,8 +246,39 @@ static int launch_rope(const void* x, void* y, int32_t b, int32_t H, int32_t n, 
   if (blocks > 65536) blocks = 65536;
   rope_kernel<T, D><<<(unsigned)blocks, 256, 0, stream>>>(
       static_cast<const T*>(x), static_cast<T*>(y), H, n, xs, ys, pos, L_meta, tok0, total, inv,
-      theta > 0.f ? 1 : 0);
+      theta > 0.f ? 1 : 0, row0, y_rows, status);
   return hip_check(hipGetLastError(), "rope_apply: launch");
+}
+
+static int rope_common(const char* who, const void* x, void* y, int32_t b, int32_t H, int32_t n,
+                       int64_t x_stride_bh, int64_t y_stride_bh, int32_t d_head, sckv_dtype dt,
+                       const int32_t* pos, int32_t L_meta, int32_t tok0, float theta,
+                       const int32_t* row0, int32_t y_rows, int32_t* status, hipStream_t stream) {
+  const std::string w(who);
+  if (!x || !y) return fail(SCKV_EINVAL, w + ": null pointer");
+  if (!valid_dtype(dt)) return fail(SCKV_EINVAL, w + ": unknown dtype");
+  if (!supported_d(d_head)) return fail(SCKV_EUNSUP, w + ": d_head must be 64 or 80");
+  if (b <= 0 || H <= 0 || n < 0) return fail(SCKV_EINVAL, w + ": bad sizes");
+  if (x_stride_bh < (int64_t)n * d_head)
+    return fail(SCKV_EINVAL, w + ": x slice stride smaller than n*d_head");
+  if (row0 ? (y_rows < n || y_stride_bh < (int64_t)y_rows * d_head)
+           : y_stride_bh < (int64_t)n * d_head)
+    return fail(SCKV_EINVAL, w + ": y slice smaller than its rows");
+  if (!(theta >= 0.f) || std::isinf(theta)) return fail(SCKV_EINVAL, w + ": theta must be finite and >= 0");
+  if (theta > 0.f) {
+    if (!pos) return fail(SCKV_EINVAL, w + ": null pos");
+    if (tok0 < 0 || L_meta <= 0 || (int64_t)tok0 + n > L_meta)
+      return fail(SCKV_EINVAL, w + ": rows [tok0, tok0+n) exceed L_meta");
+  }
+  if (!aligned16(x) || !aligned16(y) || (x_stride_bh * elem_bytes(dt)) % 16 ||
+      (y_stride_bh * elem_bytes(dt)) % 16)
+    return fail(SCKV_EINVAL, w + ": buffers and strides must be 16-byte aligned");
+  if (n == 0) return SCKV_OK;
+  if (dt == SCKV_BF16)
+    return d_head == 64 ? launch_rope<uint16_t, 64>(x, y, b, H, n, x_stride_bh, y_stride_bh, pos, L_meta, tok0, theta, row0, y_rows, status, stream)
+                        : launch_rope<uint16_t, 80>(x, y, b, H, n, x_stride_bh, y_stride_bh, pos, L_meta, tok0, theta, row0, y_rows, status, stream);
+  return d_head == 64 ? launch_rope<float, 64>(x, y, b, H, n, x_stride_bh, y_stride_bh, pos, L_meta, tok0, theta, row0, y_rows, status, stream)
+                      : launch_rope<float, 80>(x, y, b, H, n, x_stride_bh, y_stride_bh, pos, L_meta, tok0, theta, row0, y_rows, status, stream);
 }
 
 extern "C" int rope_apply(const void* x, void* y, int32_t b, int32_t H, int32_t n,
@@ -214,27 +286,33 @@ extern "C" int rope_apply(const void* x, void* y, int32_t b, int32_t H, int32_t 
                           const int32_t* pos, int32_t L_meta, int32_t tok0, float theta,
                           hipStream_t stream) {
   clear_error();
-  if (!x || !y) return fail(SCKV_EINVAL, "rope_apply: null pointer");
-  if (!valid_dtype(dt)) return fail(SCKV_EINVAL, "rope_apply: unknown dtype");
-  if (!supported_d(d_head)) return fail(SCKV_EUNSUP, "rope_apply: d_head must be 64 or 80");
-  if (b <= 0 || H <= 0 || n < 0) return fail(SCKV_EINVAL, "rope_apply: bad sizes");
-  if (x_stride_bh < (int64_t)n * d_head || y_stride_bh < (int64_t)n * d_head)
-    return fail(SCKV_EINVAL, "rope_apply: slice stride smaller than n*d_head");
-  if (!(theta >= 0.f) || std::isinf(theta)) return fail(SCKV_EINVAL, "rope_apply: theta must be finite and >= 0");
-  if (theta > 0.f) {
-    if (!pos) return fail(SCKV_EINVAL, "rope_apply: null pos");
-    if (tok0 < 0 || L_meta <= 0 || (int64_t)tok0 + n > L_meta)
-      return fail(SCKV_EINVAL, "rope_apply: rows [tok0, tok0+n) exceed L_meta");
-  }
-  if (!aligned16(x) || !aligned16(y) || (x_stride_bh * elem_bytes(dt)) % 16 ||
-      (y_stride_bh * elem_bytes(dt)) % 16)
-    return fail(SCKV_EINVAL, "rope_apply: buffers and strides must be 16-byte aligned");
-  if (n == 0) return SCKV_OK;
-  if (dt == SCKV_BF16)
-    return d_head == 64 ? launch_rope<uint16_t, 64>(x, y, b, H, n, x_stride_bh, y_stride_bh, pos, L_meta, tok0, theta, stream)
-                        : launch_rope<uint16_t, 80>(x, y, b, H, n, x_stride_bh, y_stride_bh, pos, L_meta, tok0, theta, stream);
-  return d_head == 64 ? launch_rope<float, 64>(x, y, b, H, n, x_stride_bh, y_stride_bh, pos, L_meta, tok0, theta, stream)
-                      : launch_rope<float, 80>(x, y, b, H, n, x_stride_bh, y_stride_bh, pos, L_meta, tok0, theta, stream);
+  return rope_common("rope_apply", x, y, b, H, n, x_stride_bh, y_stride_bh, d_head, dt, pos,
+                     L_meta, tok0, theta, nullptr, 0, nullptr, stream);
+}
+
+extern "C" int rope_apply_at(const void* x, void* y, const int32_t* row0, int32_t y_rows,
+                             int32_t b, int32_t H, int32_t n, int64_t x_stride_bh,
+                             int64_t y_stride_bh, int32_t d_head, sckv_dtype dt,
+                             const int32_t* pos, int32_t L_meta, int32_t tok0, float theta,
+                             int32_t* status, hipStream_t stream) {
+  clear_error();
+  if (!row0) return fail(SCKV_EINVAL, "rope_apply_at: null row0");
+  return rope_common("rope_apply_at", x, y, b, H, n, x_stride_bh, y_stride_bh, d_head, dt, pos,
+                     L_meta, tok0, theta, row0, y_rows, status, stream);
+}
+
+extern "C" int kv_extend(int32_t* kv_len, int32_t* tok_idx, int32_t* pos_ids, int32_t* row0_out,
+                         const int32_t* pos, int32_t L_meta, int32_t tok0, int32_t n, int32_t b,
+                         int32_t L_cap, int32_t* status, hipStream_t stream) {
+  clear_error();
+  if (!kv_len || !tok_idx || !pos_ids || !row0_out || !pos)
+    return fail(SCKV_EINVAL, "kv_extend: null pointer");
+  if (b <= 0 || L_cap <= 0 || L_meta <= 0 || n < 0) return fail(SCKV_EINVAL, "kv_extend: bad sizes");
+  if (tok0 < 0 || (int64_t)tok0 + n > L_meta)
+    return fail(SCKV_EINVAL, "kv_extend: tokens [tok0, tok0+n) exceed L_meta");
+  extend_kernel<<<b, 256, 0, stream>>>(kv_len, tok_idx, pos_ids, row0_out, pos, L_meta, tok0, n,
+                                       L_cap, status);
+  return hip_check(hipGetLastError(), "kv_extend: launch");
 }
 
 extern "C" int kv_commit(int32_t* kv_len, int32_t* tok_idx, int32_t* pos_ids, int32_t* cur_tok,

@@ -20,6 +20,15 @@
 //   not entirely visible to a wave; a tile entirely in a wave's future is
 //   skipped.  A <CL> row's output is its own value row (it sees only itself),
 //   written directly in the epilogue.
+//
+// Cached variant (block-wise prompt processing, Section 3 "Manipulating
+// Key-Value Memory": enclosed tokens are freed block by block when a prompt
+// does not fit): the queries are a block of the prompt, tokens tok0 .. tok0+nq-1,
+// and the keys are the rows of a cache, row r holding token tok[r] (rows of
+// earlier blocks that survived compaction, then the block's own rows from
+// row0).  The plan lists cache rows instead of columns, with the same
+// visibility rule applied to their tokens; the kernel gathers by row and
+// masks by token.
 #include <math.h>
 
 #include <cmath>
@@ -40,17 +49,38 @@ constexpr float PF_LOG2E = 1.4426950408889634f;
 // maximum, which is exact and keeps them below 2^PF_RESCALE.
 constexpr float PF_RESCALE = 8.f;
 
+// Cached variant's arguments (unused by the plain prefill).
+struct PfCached {
+  const int32_t* row0;   // [b] cache row of the block's first query token
+  const int32_t* tok;    // [b][L_cap] token held by each cache row
+  uint32_t* rows;        // plan output: cache row of each list entry
+  int32_t tok0;          // token of the block's first query
+  int32_t L_cap;
+  int32_t* status;       // nullable: SCKV_STATUS_CAP for a block that does not fit
+};
+
+// Plain: columns j < min(I+128, L) with token j.  Cached: cache rows
+// r < row0 + min(I_loc+128, nq) with token tok[r], where I_loc is the query
+// block's first local row and I = tok0 + I_loc its first token.
+template <bool CACHED>
 __global__ __launch_bounds__(256) void prefill_plan_kernel(const int32_t* __restrict__ vu,
                                                            int32_t L_meta, int32_t L, int32_t n_qt,
                                                            int32_t L_pad,
                                                            uint32_t* __restrict__ list,
-                                                           int32_t* __restrict__ count) {
+                                                           int32_t* __restrict__ count,
+                                                           PfCached cc) {
   const int qt = blockIdx.x;
   const int s = blockIdx.y;
   const int tid = threadIdx.x;
   const int wave = tid >> 6;
-  const int I = qt * PF_BQ;
-  const int jend = min(I + PF_BQ, L);
+  const int I_loc = qt * PF_BQ;
+  int I = I_loc, jend = min(I_loc + PF_BQ, L);
+  if constexpr (CACHED) {
+    I = cc.tok0 + I_loc;
+    const int r0 = cc.row0[s];
+    const bool fits = r0 >= 0 && (int64_t)r0 + L <= cc.L_cap;
+    jend = fits ? r0 + min(I_loc + PF_BQ, L) : 0;
+  }
   const int32_t* v = vu + (int64_t)s * L_meta;
   uint32_t* out = list + ((int64_t)s * n_qt + qt) * L_pad;
   __shared__ int wave_cnt[4];
@@ -60,10 +90,15 @@ __global__ __launch_bounds__(256) void prefill_plan_kernel(const int32_t* __rest
     bool ok = false;
     uint32_t e = 0;
     if (j < jend) {
-      const int x = v[j];
-      ok = x >= I;
-      const int64_t rel = (int64_t)x - I;
-      e = (uint32_t)j | ((uint32_t)(rel > 255 ? 255 : rel) << 24);
+      // the column's token: the row itself, or the token a cache row holds
+      // (a row whose token lies outside [0, L_meta) is never listed)
+      const int t = CACHED ? cc.tok[(int64_t)s * cc.L_cap + j] : j;
+      if (!CACHED || (t >= 0 && t < L_meta)) {
+        const int x = v[t];
+        ok = x >= I;
+        const int64_t rel = (int64_t)x - I;
+        e = (uint32_t)t | ((uint32_t)(rel > 255 ? 255 : rel) << 24);
+      }
     }
     const uint64_t m = __ballot(ok);
     if ((tid & 63) == 0) wave_cnt[wave] = __popcll(m);
@@ -75,7 +110,10 @@ __global__ __launch_bounds__(256) void prefill_plan_kernel(const int32_t* __rest
       if (w < wave) off += c;
       total += c;
     }
-    if (ok) out[off + mask_rank(m)] = e;
+    if (ok) {
+      out[off + mask_rank(m)] = e;
+      if constexpr (CACHED) cc.rows[((int64_t)s * n_qt + qt) * L_pad + off + mask_rank(m)] = j;
+    }
     carry += total;
     __syncthreads();
   }
@@ -134,12 +172,13 @@ typedef __attribute__((address_space(3))) void* lds_ptr_t;
 // ---------------------------------------------------------------------------
 // main kernel
 // ---------------------------------------------------------------------------
-template <typename T, int D>
+template <typename T, int D, bool CACHED>
 __device__ __forceinline__ void prefill_attn_body(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v, T* __restrict__ o,
     int32_t H, int32_t L, int64_t qs, int64_t kvs, int64_t os, float c2,
     const int32_t* __restrict__ vu, int32_t L_meta, const uint32_t* __restrict__ list,
-    const int32_t* __restrict__ count, int32_t n_qt, int32_t L_pad, int32_t n_work) {
+    const int32_t* __restrict__ count, int32_t n_qt, int32_t L_pad, int32_t n_work,
+    PfCached cc) {
   using C = PfCfg<T, D>;
   using TL = PfTile<T, D>;
   constexpr bool BF = sizeof(T) == 2;
@@ -164,21 +203,43 @@ __device__ __forceinline__ void prefill_attn_body(
   const int bh = work / n_qt;
   const int qt = n_qt - 1 - (work % n_qt);
   const int s = bh / H;
-  const int I = qt * PF_BQ;
+  // query rows are local (0 .. L-1); their tokens start at tok0 (cached) or 0
+  const int tok0 = CACHED ? cc.tok0 : 0;
+  const int I_loc = qt * PF_BQ;
+  const int I = tok0 + I_loc;
 
   const int tid = threadIdx.x;
   const int wave = tid >> 6;
   const int lane = tid & 63;
   const int l32 = lane & 31;
   const int g = lane >> 5;
+  const int Iw_loc = I_loc + wave * 32;
   const int Iw = I + wave * 32;
-  const int qrow = Iw + l32;
-  const bool wave_live = Iw < L;
+  const int qrow = Iw_loc + l32;  // local query row
+  const int qtok = Iw + l32;      // its token
+  const bool wave_live = Iw_loc < L;
 
   const T* qb = q + (int64_t)bh * qs;
   const T* kb = k + (int64_t)bh * kvs;
   const T* vb = v + (int64_t)bh * kvs;
   const uint32_t* ents = list + ((int64_t)s * n_qt + qt) * L_pad;
+  const uint32_t* rws = CACHED ? cc.rows + ((int64_t)s * n_qt + qt) * L_pad : nullptr;
+  int own_row0 = 0;  // cache row of local query row 0
+  if constexpr (CACHED) {
+    own_row0 = cc.row0[s];
+    if (own_row0 < 0 || (int64_t)own_row0 + L > cc.L_cap) {
+      // the block's rows are not in the cache: NaN outputs, nothing read
+      if (cc.status && tid == 0 && qt == 0 && (bh % H) == 0) atomicOr(cc.status, SCKV_STATUS_CAP);
+      if (wave_live && qrow < L) {
+        T* orow = o + (int64_t)bh * os + (int64_t)qrow * D;
+        for (int e = g; e < D; e += 2) {
+          if constexpr (sizeof(T) == 2) orow[e] = (T)0x7fc0;
+          else orow[e] = NAN;
+        }
+      }
+      return;
+    }
+  }
   const int n_vis = count[(int64_t)s * n_qt + qt];
   const int nt = (n_vis + PF_BK - 1) / PF_BK;
 
@@ -227,9 +288,12 @@ __device__ __forceinline__ void prefill_attn_body(
   // key/value rows of tile kt+1 go global -> LDS by direct loads addressed
   // from the ring while tile kt is multiplied ----
   uint32_t ereg = PF_NONE;
+  int rreg = 0;  // cached: the entry's cache row
   auto nvalid_of = [&](int kt) { return min(PF_BK, n_vis - kt * PF_BK); };
   auto load_entries = [&](int kt) {
-    ereg = (tid < PF_BK && tid < nvalid_of(kt)) ? ents[kt * PF_BK + tid] : PF_NONE;
+    const bool in = tid < PF_BK && tid < nvalid_of(kt);
+    ereg = in ? ents[kt * PF_BK + tid] : PF_NONE;
+    if constexpr (CACHED) rreg = in ? (int)rws[kt * PF_BK + tid] : 0;
   };
   auto store_entries = [&](int kt) {
     const int slot = kt % PF_ER;
@@ -242,7 +306,12 @@ __device__ __forceinline__ void prefill_attn_body(
       const int jmax = __shfl((int)(ereg & 0x00ffffffu), nvalid - 1, 64);
       // a padding row of the tile repeats the last valid row (its score is
       // masked, so any finite row will do)
-      row_ring[slot][tid] = tid < nvalid ? (int)(ereg & 0x00ffffffu) : jmax;
+      if constexpr (CACHED) {
+        const int rlast = __shfl(rreg, nvalid - 1, 64);
+        row_ring[slot][tid] = tid < nvalid ? rreg : rlast;
+      } else {
+        row_ring[slot][tid] = tid < nvalid ? (int)(ereg & 0x00ffffffu) : jmax;
+      }
       if (tid == 0) {
         TileInfo ti;
         ti.jmin = (int)(ereg & 0x00ffffffu);
@@ -313,7 +382,7 @@ __device__ __forceinline__ void prefill_attn_body(
       }
       // ---- element mask on tiles not entirely visible to this wave ----
       if (!full) {
-        const int ir = qrow - I;
+        const int ir = qtok - I;
 #pragma unroll
         for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
@@ -322,7 +391,7 @@ __device__ __forceinline__ void prefill_attn_body(
             const uint32_t e = tent[key];
             const int j = (int)(e & 0x00ffffffu);
             const int vr = (int)(e >> 24);
-            const bool vis = (j <= qrow) & (ir <= vr);
+            const bool vis = (j <= qtok) & (ir <= vr);
             sacc[kb2][vv] = vis ? sacc[kb2][vv] : -INFINITY;
           }
       }
@@ -448,9 +517,9 @@ __device__ __forceinline__ void prefill_attn_body(
   }
   if (qrow >= L) return;
   const float inv = 1.f / l_tot;
-  const bool is_cl = vu[(int64_t)s * L_meta + qrow] == qrow;
+  const bool is_cl = vu[(int64_t)s * L_meta + qtok] == qtok;
   T* orow = o + (int64_t)bh * os + (int64_t)qrow * D;
-  const T* vrow = vb + (int64_t)qrow * D;
+  const T* vrow = vb + (int64_t)(own_row0 + qrow) * D;
 #pragma unroll
   for (int db = 0; db < NDB; ++db)
 #pragma unroll
@@ -481,51 +550,71 @@ __device__ __forceinline__ void prefill_attn_body(
 
 // bf16 runs at three waves per SIMD (at most 168 registers), measured faster
 // than two and than four; the fp32 variant (small parity cases) is not capped.
-template <int D>
+template <int D, bool CACHED>
 __global__ __launch_bounds__(PF_THREADS) __attribute__((amdgpu_waves_per_eu(3))) void prefill_attn_kernel_bf16(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     uint16_t* __restrict__ o, int32_t H, int32_t L, int64_t qs, int64_t kvs, int64_t os, float c2,
     const int32_t* __restrict__ vu, int32_t L_meta, const uint32_t* __restrict__ list,
-    const int32_t* __restrict__ count, int32_t n_qt, int32_t L_pad, int32_t n_work) {
-  prefill_attn_body<uint16_t, D>(q, k, v, o, H, L, qs, kvs, os, c2, vu, L_meta, list, count, n_qt,
-                                 L_pad, n_work);
+    const int32_t* __restrict__ count, int32_t n_qt, int32_t L_pad, int32_t n_work, PfCached cc) {
+  prefill_attn_body<uint16_t, D, CACHED>(q, k, v, o, H, L, qs, kvs, os, c2, vu, L_meta, list,
+                                         count, n_qt, L_pad, n_work, cc);
 }
 
-template <int D>
+template <int D, bool CACHED>
 __global__ __launch_bounds__(PF_THREADS) void prefill_attn_kernel_f32(
     const float* __restrict__ q, const float* __restrict__ k, const float* __restrict__ v,
     float* __restrict__ o, int32_t H, int32_t L, int64_t qs, int64_t kvs, int64_t os, float c2,
     const int32_t* __restrict__ vu, int32_t L_meta, const uint32_t* __restrict__ list,
-    const int32_t* __restrict__ count, int32_t n_qt, int32_t L_pad, int32_t n_work) {
-  prefill_attn_body<float, D>(q, k, v, o, H, L, qs, kvs, os, c2, vu, L_meta, list, count, n_qt,
-                              L_pad, n_work);
+    const int32_t* __restrict__ count, int32_t n_qt, int32_t L_pad, int32_t n_work, PfCached cc) {
+  prefill_attn_body<float, D, CACHED>(q, k, v, o, H, L, qs, kvs, os, c2, vu, L_meta, list, count,
+                                      n_qt, L_pad, n_work, cc);
 }
 
-template <typename T, int D>
+template <typename T, int D, bool CACHED>
 static int launch_prefill(const void* q, const void* k, const void* v, void* o, int32_t b,
                           int32_t H, int32_t L, int64_t qs, int64_t kvs, int64_t os, float scale,
                           const int32_t* vu, int32_t L_meta, uint32_t* list, int32_t* count,
-                          int32_t n_qt, int32_t L_pad, hipStream_t stream) {
-  prefill_plan_kernel<<<dim3(n_qt, b), 256, 0, stream>>>(vu, L_meta, L, n_qt, L_pad, list, count);
+                          int32_t n_qt, int32_t L_pad, PfCached cc, hipStream_t stream) {
+  prefill_plan_kernel<CACHED><<<dim3(n_qt, b), 256, 0, stream>>>(vu, L_meta, L, n_qt, L_pad, list,
+                                                                 count, cc);
   int rc = hip_check(hipGetLastError(), "span_masked_prefill_attn: plan launch");
   if (rc) return rc;
   const int n_work = b * H * n_qt;
   if constexpr (sizeof(T) == 2)
-    prefill_attn_kernel_bf16<D><<<n_work, PF_THREADS, 0, stream>>>(
+    prefill_attn_kernel_bf16<D, CACHED><<<n_work, PF_THREADS, 0, stream>>>(
         static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
         static_cast<T*>(o), H, L, qs, kvs, os, scale * PF_LOG2E, vu, L_meta, list, count, n_qt,
-        L_pad, n_work);
+        L_pad, n_work, cc);
   else
-    prefill_attn_kernel_f32<D><<<n_work, PF_THREADS, 0, stream>>>(
+    prefill_attn_kernel_f32<D, CACHED><<<n_work, PF_THREADS, 0, stream>>>(
         static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
         static_cast<T*>(o), H, L, qs, kvs, os, scale * PF_LOG2E, vu, L_meta, list, count, n_qt,
-        L_pad, n_work);
+        L_pad, n_work, cc);
   return hip_check(hipGetLastError(), "span_masked_prefill_attn: launch");
+}
+
+template <bool CACHED>
+static int dispatch_prefill(const void* q, const void* k, const void* v, void* o, int32_t b,
+                            int32_t H, int32_t L, int32_t d_head, sckv_dtype dt, int64_t qs,
+                            int64_t kvs, int64_t os, float scale, const int32_t* vu,
+                            int32_t L_meta, uint32_t* list, int32_t* cnt, int32_t n_qt,
+                            int32_t L_pad, PfCached cc, hipStream_t stream) {
+  if (dt == SCKV_BF16)
+    return d_head == 64 ? launch_prefill<uint16_t, 64, CACHED>(q, k, v, o, b, H, L, qs, kvs, os, scale, vu, L_meta, list, cnt, n_qt, L_pad, cc, stream)
+                        : launch_prefill<uint16_t, 80, CACHED>(q, k, v, o, b, H, L, qs, kvs, os, scale, vu, L_meta, list, cnt, n_qt, L_pad, cc, stream);
+  return d_head == 64 ? launch_prefill<float, 64, CACHED>(q, k, v, o, b, H, L, qs, kvs, os, scale, vu, L_meta, list, cnt, n_qt, L_pad, cc, stream)
+                      : launch_prefill<float, 80, CACHED>(q, k, v, o, b, H, L, qs, kvs, os, scale, vu, L_meta, list, cnt, n_qt, L_pad, cc, stream);
 }
 
 static void plan_geometry(int32_t L, int32_t* n_qt, int32_t* L_pad) {
   *n_qt = (L + PF_BQ - 1) / PF_BQ;
   *L_pad = *n_qt * PF_BQ;
+}
+
+// cached: a query block lists at most row0 + nq <= L_cap rows
+static void plan_geometry_cached(int32_t nq, int32_t L_cap, int32_t* n_qt, int32_t* L_pad) {
+  *n_qt = (nq + PF_BQ - 1) / PF_BQ;
+  *L_pad = (L_cap + PF_BQ - 1) / PF_BQ * PF_BQ;
 }
 
 }  // namespace sckv
@@ -569,9 +658,65 @@ extern "C" int span_masked_prefill_attn(const void* q, const void* k, const void
   if ((int64_t)b * H * n_qt > 0x7fffffff) return fail(SCKV_EUNSUP, "span_masked_prefill_attn: grid too large");
   uint32_t* list = static_cast<uint32_t*>(ws);
   int32_t* cnt = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + (size_t)b * n_qt * L_pad * sizeof(uint32_t));
-  if (dt == SCKV_BF16)
-    return d_head == 64 ? launch_prefill<uint16_t, 64>(q, k, v, o, b, H, L, q_stride_bh, kv_stride_bh, o_stride_bh, scale, vu, L_meta, list, cnt, n_qt, L_pad, stream)
-                        : launch_prefill<uint16_t, 80>(q, k, v, o, b, H, L, q_stride_bh, kv_stride_bh, o_stride_bh, scale, vu, L_meta, list, cnt, n_qt, L_pad, stream);
-  return d_head == 64 ? launch_prefill<float, 64>(q, k, v, o, b, H, L, q_stride_bh, kv_stride_bh, o_stride_bh, scale, vu, L_meta, list, cnt, n_qt, L_pad, stream)
-                      : launch_prefill<float, 80>(q, k, v, o, b, H, L, q_stride_bh, kv_stride_bh, o_stride_bh, scale, vu, L_meta, list, cnt, n_qt, L_pad, stream);
+  return dispatch_prefill<false>(q, k, v, o, b, H, L, d_head, dt, q_stride_bh, kv_stride_bh,
+                                 o_stride_bh, scale, vu, L_meta, list, cnt, n_qt, L_pad,
+                                 PfCached{}, stream);
+}
+
+extern "C" size_t sckv_prefill_cached_workspace_bytes(int32_t b, int32_t nq, int32_t L_cap) {
+  if (b <= 0 || nq <= 0 || L_cap <= 0) return 0;
+  int32_t n_qt, L_pad;
+  plan_geometry_cached(nq, L_cap, &n_qt, &L_pad);
+  const size_t list = (size_t)b * n_qt * L_pad * sizeof(uint32_t);  // entries, then rows
+  const size_t cnt = ((size_t)b * n_qt * sizeof(int32_t) + 255) / 256 * 256;
+  return 2 * list + cnt;
+}
+
+extern "C" int span_masked_prefill_attn_cached(
+    const void* q, const void* k_cache, const void* v_cache, void* o, int32_t b, int32_t H,
+    int32_t nq, int32_t d_head, int64_t q_stride_bh, int64_t kv_stride_bh, int64_t o_stride_bh,
+    sckv_dtype dt, float scale, const int32_t* vu, int32_t L_meta, int32_t tok0,
+    const int32_t* row0, const int32_t* tok_idx, int32_t L_cap, void* ws, size_t ws_bytes,
+    int32_t* status, hipStream_t stream) {
+  clear_error();
+  const char* W = "span_masked_prefill_attn_cached";
+  if (!q || !k_cache || !v_cache || !o || !vu || !row0 || !tok_idx || !ws)
+    return fail(SCKV_EINVAL, std::string(W) + ": null pointer");
+  if (!valid_dtype(dt)) return fail(SCKV_EINVAL, std::string(W) + ": unknown dtype");
+  if (!supported_d(d_head)) return fail(SCKV_EUNSUP, std::string(W) + ": d_head must be 64 or 80");
+  if (b <= 0 || H <= 0 || nq <= 0 || L_cap <= 0)
+    return fail(SCKV_EINVAL, std::string(W) + ": sizes must be positive");
+  if (L_cap > 32768 || nq > L_cap) return fail(SCKV_EUNSUP, std::string(W) + ": nq <= L_cap <= 32768 required");
+  // list entries hold a token in 24 bits; 0xffffff marks padding
+  if (L_meta <= 0 || L_meta >= (int32_t)PF_NONE)
+    return fail(SCKV_EUNSUP, std::string(W) + ": L_meta must be in (0, 2^24 - 1)");
+  if (tok0 < 0 || (int64_t)tok0 + nq > L_meta)
+    return fail(SCKV_EINVAL, std::string(W) + ": query tokens [tok0, tok0+nq) exceed L_meta");
+  if (q_stride_bh < (int64_t)nq * d_head || o_stride_bh < (int64_t)nq * d_head ||
+      kv_stride_bh < (int64_t)L_cap * d_head)
+    return fail(SCKV_EINVAL, std::string(W) + ": slice stride too small");
+  const int eb = elem_bytes(dt);
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(o) ||
+      !aligned16(ws) || (q_stride_bh * eb) % 16 || (kv_stride_bh * eb) % 16 ||
+      (o_stride_bh * eb) % 16)
+    return fail(SCKV_EINVAL, std::string(W) + ": buffers and strides must be 16-byte aligned");
+  if (!(scale > 0.f) || std::isinf(scale)) return fail(SCKV_EINVAL, std::string(W) + ": scale must be finite and > 0");
+  if (ws_bytes < sckv_prefill_cached_workspace_bytes(b, nq, L_cap))
+    return fail(SCKV_EINVAL, std::string(W) + ": workspace too small");
+  int32_t n_qt, L_pad;
+  plan_geometry_cached(nq, L_cap, &n_qt, &L_pad);
+  if ((int64_t)b * H * n_qt > 0x7fffffff) return fail(SCKV_EUNSUP, std::string(W) + ": grid too large");
+  const size_t list_bytes = (size_t)b * n_qt * L_pad * sizeof(uint32_t);
+  uint32_t* list = static_cast<uint32_t*>(ws);
+  PfCached cc;
+  cc.rows = reinterpret_cast<uint32_t*>(static_cast<char*>(ws) + list_bytes);
+  cc.row0 = row0;
+  cc.tok = tok_idx;
+  cc.tok0 = tok0;
+  cc.L_cap = L_cap;
+  cc.status = status;
+  int32_t* cnt = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + 2 * list_bytes);
+  return dispatch_prefill<true>(q, k_cache, v_cache, o, b, H, nq, d_head, dt, q_stride_bh,
+                                kv_stride_bh, o_stride_bh, scale, vu, L_meta, list, cnt, n_qt,
+                                L_pad, cc, stream);
 }

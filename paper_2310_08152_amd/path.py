@@ -8,6 +8,10 @@ Typical use (one batch of sequences):
     for m in layers: prefill_layer(...)               # rotary + masked attention
     cache.compact(meta, next_tok)                     # free closed spans in place
     for step: for m: decode_layer(...); commit(...)   # generate
+
+A prompt too long for the cache is processed block by block instead
+(prefill_progressive): each block is appended to the compacted cache,
+attends to it, and the spans it closes are freed before the next block.
 """
 from __future__ import annotations
 
@@ -66,19 +70,31 @@ class KVCache:
                      self.tok_idx, self.pos_ids, nt, meta.vu, meta.L_meta, self.kept_src,
                      stream=stream)
 
+    def extend(self, meta: SpanMeta, tok0: int, n: int, row0, stream=None):
+        """Rows for prompt tokens tok0 .. tok0+n-1 after the current rows;
+        row0 (device int32 [b]) receives each sequence's first new row."""
+        B.kv_extend(self.kv_len, self.tok_idx, self.pos_ids, row0, meta.pos, meta.L_meta, tok0, n,
+                    self.b, self.L_cap, self.status, stream=stream)
+
     def commit(self, meta: SpanMeta, stream=None):
         B.kv_commit(self.kv_len, self.tok_idx, self.pos_ids, self.cur_tok, meta.vu, meta.pos,
                     meta.L_meta, self.b, self.L_cap, self.status, stream=stream)
 
 
 class Workspace:
-    """Device workspaces sized for a batch shape."""
+    """Device workspaces sized for a batch shape (block: the block size of
+    block-wise prompt processing, if used)."""
 
-    def __init__(self, b: int, H: int, L: int, L_cap: int, d: int, device):
+    def __init__(self, b: int, H: int, L: int, L_cap: int, d: int, device, block: int = 0):
         self.prefill = torch.empty(max(1, B.sckv_prefill_workspace_bytes(b, max(L, 1))),
                                    dtype=torch.uint8, device=device)
         self.decode = torch.empty(max(1, B.sckv_decode_workspace_bytes(b, H, L_cap, d)),
                                   dtype=torch.uint8, device=device)
+        self.prefill_cached = None
+        if block > 0:
+            self.prefill_cached = torch.empty(
+                max(1, B.sckv_prefill_cached_workspace_bytes(b, block, L_cap)),
+                dtype=torch.uint8, device=device)
 
 
 def default_scale(d: int) -> float:
@@ -107,3 +123,53 @@ def decode_layer(q, k_new, v_new, cache: KVCache, m: int, meta: SpanMeta, ws: Wo
                             meta.vu, meta.pos, meta.L_meta, o, cache.b, cache.H, cache.L_cap, d,
                             default_scale(d) if scale is None else scale, theta, ws.decode,
                             cache.status, stream=stream)
+
+
+def prefill_block(q, cache: KVCache, m: int, o, meta: SpanMeta, ws: Workspace, tok0: int, row0,
+                  scale=None, stream=None):
+    """Masked attention of a block's queries q (b,H,nq,d), tokens tok0.., over
+    layer m of the cache, whose rows row0.. hold the block itself."""
+    b, H, nq, d = q.shape
+    B.span_masked_prefill_attn_cached(q, cache.k(m), cache.v(m), o, b, H, nq, d, q.stride(1),
+                                      cache.k(m).stride(1), o.stride(1),
+                                      default_scale(d) if scale is None else scale, meta.vu,
+                                      meta.L_meta, tok0, row0, cache.tok_idx, cache.L_cap,
+                                      ws.prefill_cached, status=cache.status, stream=stream)
+
+
+def prefill_progressive(q, k, v, o, cache: KVCache, meta: SpanMeta, ws: Workspace, L: int,
+                        block: int, theta: float = 0.0, scale=None, stream=None,
+                        on_block=None):
+    """Process the prompt (tokens 0..L-1) in blocks of `block` tokens:
+    for each block, append its rows to the compacted cache (keys rotated),
+    run the masked attention of its queries over the cache for every layer,
+    then free the spans closed within it (compaction at the block's end).
+
+    q, k, v, o: (M, b, H, >= L, d) per-layer prompt tensors (o receives the
+    outputs).  The cache starts empty; at the end it holds the rows a token
+    after the prompt may see, exactly as a one-shot prefill + compaction
+    leaves it.  on_block(B1), if given, is called after each block."""
+    M, b, H, _, d = q.shape
+    cache.kv_len.zero_()
+    row0 = torch.empty(b, dtype=torch.int32, device=q.device)
+    nxt = torch.empty(b, dtype=torch.int32, device=q.device)
+    qr = torch.empty(b, H, block, d, dtype=q.dtype, device=q.device)
+    for B0 in range(0, L, block):
+        n = min(block, L - B0)
+        cache.extend(meta, B0, n, row0, stream=stream)
+        for m in range(M):
+            for kv, src, th in ((0, k, theta), (1, v, 0.0)):
+                x = src[m, :, :, B0:B0 + n]
+                dst = cache.kv[m, kv]
+                B.rope_apply_at(x, dst, row0, cache.L_cap, b, H, n, x.stride(1), dst.stride(1), d,
+                                meta.pos, meta.L_meta, B0, th, status=cache.status,
+                                stream=stream)
+            B.rope_apply(q[m, :, :, B0:B0 + n], qr, b, H, n, q.stride(2), qr.stride(1), d,
+                         meta.pos, meta.L_meta, B0, theta, stream=stream)
+            prefill_block(qr[:, :, :n], cache, m, o[m, :, :, B0:B0 + n], meta, ws, B0, row0,
+                          scale=scale, stream=stream)
+        nxt.fill_(B0 + n)
+        cache.compact(meta, next_tok=nxt, stream=stream)
+        if on_block is not None:
+            on_block(B0 + n)
+    cache.cur_tok.fill_(L)

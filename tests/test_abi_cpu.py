@@ -138,3 +138,43 @@ def test_binding_raises_with_message(B):
         B.sckv_span_meta(np.array([[5, 10]]), np.array([[10, 20]]), np.array([2]), 100,
                          None, None)
     assert e.value.code == B.EINVAL or e.value.code == B.ESPAN
+
+
+def test_block_entry_points_reject_bad_arguments(B):
+    """Block-wise prompt processing: rope_apply_at, kv_extend and
+    span_masked_prefill_attn_cached check their arguments on the host."""
+    lib = B.lib
+    # rope_apply_at: null row0, y slice smaller than its rows, tokens past L_meta
+    assert lib.rope_apply_at(FAKE, FAKE, NULL, 64, 1, 1, 8, 8 * 64, 64 * 64, 64, B.BF16, FAKE,
+                             100, 0, 1e4, NULL, NULL) == B.EINVAL
+    assert lib.rope_apply_at(FAKE, FAKE, FAKE, 64, 1, 1, 8, 8 * 64, 32 * 64, 64, B.BF16, FAKE,
+                             100, 0, 1e4, NULL, NULL) == B.EINVAL
+    assert lib.rope_apply_at(FAKE, FAKE, FAKE, 64, 1, 1, 8, 8 * 64, 64 * 64, 64, B.BF16, FAKE,
+                             100, 95, 1e4, NULL, NULL) == B.EINVAL
+    assert "L_meta" in B.last_error()
+    # kv_extend: null pos, tokens past L_meta, negative n
+    assert lib.kv_extend(FAKE, FAKE, FAKE, FAKE, NULL, 100, 0, 8, 1, 64, NULL, NULL) == B.EINVAL
+    assert lib.kv_extend(FAKE, FAKE, FAKE, FAKE, FAKE, 100, 96, 8, 1, 64, NULL, NULL) == B.EINVAL
+    assert lib.kv_extend(FAKE, FAKE, FAKE, FAKE, FAKE, 100, 0, -1, 1, 64, NULL, NULL) == B.EINVAL
+    # prefill over the cache
+    ws = lib.sckv_prefill_cached_workspace_bytes(2, 100, 512)
+    assert ws == 2 * (2 * 1 * 512 * 4) + 256  # entries + rows, one 128-query block; counts
+    assert lib.sckv_prefill_cached_workspace_bytes(0, 100, 512) == 0
+
+    def call(**kw):
+        a = dict(b=2, H=2, nq=100, d=64, qs=100 * 64, kvs=512 * 64, os=100 * 64, dt=B.BF16,
+                 scale=0.125, L_meta=1000, tok0=0, row0=FAKE, tok=FAKE, L_cap=512, ws=ws)
+        a.update(kw)
+        return lib.span_masked_prefill_attn_cached(
+            FAKE, FAKE, FAKE, FAKE, a["b"], a["H"], a["nq"], a["d"], a["qs"], a["kvs"], a["os"],
+            a["dt"], a["scale"], FAKE, a["L_meta"], a["tok0"], a["row0"], a["tok"], a["L_cap"],
+            FAKE, a["ws"], NULL, NULL)
+    assert call(row0=NULL) == B.EINVAL
+    assert call(tok=NULL) == B.EINVAL
+    assert call(nq=600) == B.EUNSUP              # nq > L_cap
+    assert call(L_meta=1 << 24) == B.EUNSUP      # tokens must fit 24 bits
+    assert call(tok0=950) == B.EINVAL            # tokens [950, 1050) past L_meta
+    assert call(kvs=256 * 64) == B.EINVAL        # cache slice smaller than L_cap rows
+    assert call(ws=ws - 1) == B.EINVAL
+    assert call(d=96) == B.EUNSUP
+    assert call(scale=0.0) == B.EINVAL

@@ -1,0 +1,161 @@
+"""Block-wise prompt processing with freeing after every block (Section 3,
+"Manipulating Key-Value Memory for Inference-time Compression"): each block
+of the prompt is appended to the compacted cache, attends to it, and the
+spans it closes are freed before the next block.
+
+Checked against the oracle's masked attention over the whole prompt, and
+against the one-shot path: after the last block the cache holds exactly the
+rows (bit for bit, with their token indices and positions) that a one-shot
+prefill followed by compaction leaves.  The cache is sized to the largest
+(surviving rows + one block), so a block that did not fit would show up as
+a status bit."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import sckv_oracle as O
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+TOL = {"bf16": 2e-2, "f32": 1e-5}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def P():
+    from paper_2310_08152_amd import path
+    return path
+
+
+def W():
+    from paper_2310_08152_amd import workload
+    return workload
+
+
+def f64(t):
+    return t.detach().to("cpu", torch.float64).numpy()
+
+
+def say(msg):
+    print(msg, flush=True)
+
+
+def spans_for(kind, b, L, rng):
+    if kind == "uniform":
+        return [W().spans_uniform_lengths(L, 0.5, 16, 64, rng) for _ in range(b)]
+    if kind == "long":  # spans longer than a block, one open at the end
+        return [[(5, 400), (401, 650), (660, L + 3)] for _ in range(b)]
+    out = []
+    for _ in range(b):  # random lengths up to 60, gaps up to 8, last span may stay open
+        sp, c = [], int(rng.integers(0, 9))
+        while c < L - 1:
+            r = c + int(rng.integers(1, 61))
+            if r >= L:
+                sp.append((c, L + 7))
+                break
+            sp.append((c, r))
+            c = r + 1 + int(rng.integers(0, 9))
+        out.append(sp)
+    return out
+
+
+CASES = [
+    # name, dtype, M, b, H, L, d, theta, block, spans
+    ("bf16-d80-rope-block128", "bf16", 2, 2, 3, 600, 80, 1e4, 128, "uniform"),
+    ("bf16-d64-block100", "bf16", 2, 2, 2, 450, 64, 0.0, 100, "random"),
+    ("f32-d64-rope-block64", "f32", 1, 2, 2, 300, 64, 1e4, 64, "random"),
+    ("f32-d80-one-block", "f32", 1, 1, 2, 300, 80, 0.0, 300, "random"),
+    ("bf16-d80-rope-block96-long-spans", "bf16", 1, 1, 2, 700, 80, 1e4, 96, "long"),
+]
+
+
+@pytest.mark.parametrize("name,dtype,M,b,H,L,d,theta,block,kind", CASES,
+                         ids=[c[0] for c in CASES])
+def test_progressive_prefill(name, dtype, M, b, H, L, d, theta, block, kind):
+    say(f"progressive prefill case={name}")
+    rng = np.random.default_rng(L + block)
+    spans = spans_for(kind, b, L, rng)
+    types = [O.token_types(sp, L) for sp in spans]
+    pos = [O.tie_positions(t) for t in types]
+    # largest cache the block-wise path needs: survivors before a block + the block
+    peak = 0
+    for B0 in range(0, L, block):
+        n = min(block, L - B0)
+        for s in range(b):
+            kept = int(O.keep_rows(types[s], B0)[:B0].sum()) if B0 else 0
+            peak = max(peak, kept + n)
+    L_cap = peak
+    assert L_cap < L or block >= L
+    dt = W().torch_dtype(dtype)
+    shp = (M, b, H, L, d)
+    q, k, v = (W().randn(shp, seed=700 + i, dtype=dtype, device=DEV) for i in range(3))
+    meta = P().SpanMeta(spans, L, DEV)
+    cache = P().KVCache(M, b, H, L_cap, d, dt, DEV)
+    ws = P().Workspace(b, H, block, L_cap, d, DEV, block=block)
+    o = torch.full_like(q, float("nan"))
+    rows_seen = []
+    P().prefill_progressive(q, k, v, o, cache, meta, ws, L, block, theta=theta,
+                            on_block=lambda B1: rows_seen.append(cache.kv_len.clone()))
+    torch.cuda.synchronize()
+    assert int(cache.status) == 0
+    assert len(rows_seen) == (L + block - 1) // block
+
+    # outputs: the oracle over the whole prompt
+    Og, Q, K, V = f64(o), f64(q), f64(k), f64(v)
+    worst = 0.0
+    for s in range(b):
+        mask = O.attention_mask(types[s])
+        for m in range(M):
+            for h in range(H):
+                Qs, Ks = Q[m, s, h], K[m, s, h]
+                if theta > 0:
+                    Qs = O.rope_rotate_half(Qs, pos[s], theta)
+                    Ks = O.rope_rotate_half(Ks, pos[s], theta)
+                ref = O.masked_attention(Qs[None], Ks[None], V[m, s, h][None], mask)[0]
+                worst = max(worst, np.abs(Og[m, s, h] - ref).max())
+                for c, _ in spans[s]:
+                    if c < L:
+                        assert np.array_equal(Og[m, s, h, c], V[m, s, h, c]), (m, s, h, c)
+    assert np.isfinite(Og).all()
+    assert worst <= TOL[dtype], worst
+
+    # final cache: identical to one-shot rotary + compaction at the prompt's end
+    one = P().KVCache(M, b, H, L, d, dt, DEV)
+    for m in range(M):
+        P().rope_rows(k[m], one.k(m), meta, L, 0, theta)
+        one.v(m).copy_(v[m])
+    one.start_prompt(L, meta)
+    one.compact(meta)
+    torch.cuda.synchronize()
+    assert torch.equal(cache.kv_len, one.kv_len)
+    for s in range(b):
+        n = int(one.kv_len[s])
+        assert torch.equal(cache.tok_idx[s, :n], one.tok_idx[s, :n])
+        assert torch.equal(cache.pos_ids[s, :n], one.pos_ids[s, :n])
+        assert torch.equal(cache.kv[:, :, s, :, :n], one.kv[:, :, s, :, :n])
+    assert int(cache.cur_tok[0]) == L
+
+
+def test_progressive_block_without_room_reports_capacity():
+    """A block that does not fit leaves the cache as it was, sets the
+    capacity bit, and its outputs are NaN; nothing faults."""
+    say("progressive prefill without room")
+    b, H, L, d, block = 1, 1, 200, 64, 128
+    spans = [[(10, 20)]]
+    q, k, v = (W().randn((1, b, H, L, d), seed=800 + i, dtype="bf16", device=DEV)
+               for i in range(3))
+    meta = P().SpanMeta(spans, L, DEV)
+    cache = P().KVCache(1, b, H, 150, d, torch.bfloat16, DEV)  # 118 + 72 rows do not fit
+    ws = P().Workspace(b, H, block, 150, d, DEV, block=block)
+    o = torch.zeros_like(q)
+    P().prefill_progressive(q, k, v, o, cache, meta, ws, L, block)
+    torch.cuda.synchronize()
+    assert int(cache.status) & 1
+    assert int(cache.kv_len[0]) == 118  # first block only, compacted
+    assert torch.isfinite(o[0, 0, 0, :128].float()).all()
+    assert torch.isnan(o[0, 0, 0, 128:].float()).all()
