@@ -49,6 +49,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--gen-tokens", type=int, default=None,
                     help="streaming workload: generated tokens per run (default: all)")
+    ap.add_argument("--prefill-block", type=int, default=0,
+                    help="process the prompt in blocks of this many tokens, freeing closed "
+                         "spans after each block (0: one-shot prefill)")
     ap.add_argument("--span-sweep", action="store_true",
                     help="span lengths U(2,25) at each of --sweep-ratios instead of the "
                          "workload's own spans")
@@ -357,7 +360,15 @@ def measure(args, w):
     theta = w.rope_theta
     T = L + steps
     spans_all = W.workload_spans(w)
-    L_cap = max(L, max(kept_rows(s, L) for s in spans_all) + steps)
+    pb = args.prefill_block
+    L_cap_one_shot = max(L, max(kept_rows(s, L) for s in spans_all) + steps)
+    if pb > 0:
+        # block-wise prompt: the cache holds the survivors of earlier blocks
+        # plus one block, then the decode rows
+        peak = max(kept_rows(s, B0) + min(pb, L - B0) for s in spans_all for B0 in range(0, L, pb))
+        L_cap = max(peak, max(kept_rows(s, L) for s in spans_all) + steps)
+    else:
+        L_cap = L_cap_one_shot
 
     # ---- inputs resident in HBM ----
     dt = W.torch_dtype(w.dtype)
@@ -374,7 +385,7 @@ def measure(args, w):
 
     meta = P.SpanMeta(spans_all, T, dev)
     cache = P.KVCache(M, b, H, L_cap, d, dt, dev)
-    ws = P.Workspace(b, H, L, L_cap, d, dev)
+    ws = P.Workspace(b, H, L, L_cap, d, dev, block=pb)
     qr = torch.empty(b, H, L, d, dtype=dt, device=dev)
     o = torch.empty(b, H, L, d, dtype=dt, device=dev)
     od = torch.empty(b, H, d, dtype=dt, device=dev)
@@ -387,21 +398,29 @@ def measure(args, w):
     def run_step(rec):
         if rec is not None:
             rec["t0"].record()
-        cache.start_prompt(L, meta)
-        for m in range(M):
-            P.rope_rows(q_in[m], qr, meta, L, 0, theta)
-            P.rope_rows(k_in[m], cache.k(m), meta, L, 0, theta)
-            P.rope_rows(v_in[m], cache.v(m), meta, L, 0, 0.0)
-            if rec is not None and use_ev:
-                rec["pf"][m][0].record()
-            P.prefill_layer(qr, cache.k(m), cache.v(m), o, meta, ws, L)
-            if rec is not None and use_ev:
-                rec["pf"][m][1].record()
-        if rec is not None:
-            rec["t1"].record()
-        cache.compact(meta)
-        if rec is not None:
-            rec["t2"].record()
+        if pb > 0:
+            # rotary, append, masked attention and freeing, block by block
+            P.prefill_progressive(q_in, k_in, v_in, o.unsqueeze(0).expand(M, b, H, L, d), cache,
+                                  meta, ws, L, pb, theta=theta)
+            if rec is not None:
+                rec["t1"].record()
+                rec["t2"].record()
+        else:
+            cache.start_prompt(L, meta)
+            for m in range(M):
+                P.rope_rows(q_in[m], qr, meta, L, 0, theta)
+                P.rope_rows(k_in[m], cache.k(m), meta, L, 0, theta)
+                P.rope_rows(v_in[m], cache.v(m), meta, L, 0, 0.0)
+                if rec is not None and use_ev:
+                    rec["pf"][m][0].record()
+                P.prefill_layer(qr, cache.k(m), cache.v(m), o, meta, ws, L)
+                if rec is not None and use_ev:
+                    rec["pf"][m][1].record()
+            if rec is not None:
+                rec["t1"].record()
+            cache.compact(meta)
+            if rec is not None:
+                rec["t2"].record()
         for t in range(steps):
             # one event pair around the M back-to-back decode calls of a step:
             # a pair around every call would add the events' own overhead to
@@ -423,7 +442,7 @@ def measure(args, w):
     recs = []
     for _ in range(args.steps):
         recs.append({"t0": E(), "t1": E(), "t2": E(), "t3": E(),
-                     "pf": [(E(), E()) for _ in range(M)] if use_ev else None,
+                     "pf": [(E(), E()) for _ in range(M)] if use_ev and pb == 0 else None,
                      "dec": [(E(), E()) for _ in range(steps)] if use_ev else None})
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
@@ -457,7 +476,8 @@ def measure(args, w):
     decph_ms = [r["t2"].elapsed_time(r["t3"]) for r in recs]
     if use_ev:
         dec_step_ms = np.array([[a.elapsed_time(z) for a, z in r["dec"]] for r in recs])
-        pf_launch_ms = np.array([[a.elapsed_time(z) for a, z in r["pf"]] for r in recs])
+        pf_launch_ms = (np.array([[a.elapsed_time(z) for a, z in r["pf"]] for r in recs])
+                        if pb == 0 else np.array(pre_ms) / M)
         dec_total_ms = float(dec_step_ms.sum(axis=1).mean())
         dec_avg_ms = dec_total_ms / max(n_dec, 1)
         pf_avg_ms = float(pf_launch_ms.mean())
@@ -524,7 +544,8 @@ def measure(args, w):
         "phases_ms": {"rope+prefill": round(float(np.mean(pre_ms)), 3),
                       "compaction": round(float(np.mean(cmp_ms)), 3),
                       "decode": round(float(np.mean(decph_ms)), 3)},
-        "compaction_gbs": round(comp_bytes / (float(np.mean(cmp_ms)) * 1e-3) / 1e9, 1),
+        "compaction_gbs": (round(comp_bytes / (float(np.mean(cmp_ms)) * 1e-3) / 1e9, 1)
+                           if pb == 0 else None),
         "compaction_bytes": int(comp_bytes),
         "compaction_traffic": None if cmp_traffic is None else int(cmp_traffic),
         "wall_s_timed": round(wall, 3),
@@ -549,6 +570,17 @@ def measure(args, w):
                                            args.cpu_seconds)
     elt = 2 if w.dtype == "bf16" else 4
     live = int(n_keep.max()) + steps  # rows held by the longest sequence at the last step
+    if pb > 0:
+        # the prompt phase holds rotary, appends, attention and compaction of
+        # every block; prefill figures are per layer of that phase
+        out["prefill_block"] = pb
+        out["roofline_prefill"]["kernel"] = ("prompt phase per layer, block-wise: rope_apply_at + "
+                                             "span_masked_prefill_attn_cached + kv_compact")
+        out["phases_ms"]["prompt_blockwise"] = out["phases_ms"].pop("rope+prefill")
+        out["phases_ms"].pop("compaction", None)
+        out["compaction_gbs"] = out["compaction_bytes"] = out["compaction_traffic"] = None
+        out["kv_rows_capacity"] = int(L_cap)
+        out["kv_rows_capacity_one_shot"] = int(L_cap_one_shot)
     out["kv_rows_decode_max"] = live
     out["kv_bytes_decode"] = int(M * 2 * b * H * live * d * elt)
     out["kv_bytes_allocated"] = int(M * 2 * b * H * L_cap * d * elt)
