@@ -52,6 +52,9 @@ def parse():
     ap.add_argument("--prefill-block", type=int, default=0,
                     help="process the prompt in blocks of this many tokens, freeing closed "
                          "spans after each block (0: one-shot prefill)")
+    ap.add_argument("--local-attention", action="store_true",
+                    help="the local-attention comparator: decode over a ring of the W most "
+                         "recent tokens, W = the rows the compressed cache holds at its largest")
     ap.add_argument("--span-sweep", action="store_true",
                     help="span lengths U(2,25) at each of --sweep-ratios instead of the "
                          "workload's own spans")
@@ -344,6 +347,8 @@ def main():
         return run_streaming(args, w)
     if args.span_sweep:
         return run_span_sweep(args, w)
+    if args.local_attention:
+        return run_local_attention(args, w)
     print(json.dumps(measure(args, w)), flush=True)
 
 
@@ -587,6 +592,79 @@ def measure(args, w):
     out["decode_tokens_per_s"] = (round(b * steps / (float(np.mean(decph_ms)) * 1e-3), 1)
                                   if steps else None)
     return out
+
+
+def run_local_attention(args, w):
+    """Decode of the workload's shape with the local-attention comparator at an
+    equal KV budget: each token attends to the W most recent tokens, held in a
+    ring of W rows, where W is the largest row count the compressed cache
+    reaches (survivors of the prompt plus the generated tokens)."""
+    import torch
+
+    from paper_2310_08152_amd import path as P
+    from paper_2310_08152_amd import workload as W_
+
+    dev = "cuda:0"
+    steps = w.decode_steps if args.decode_steps is None else args.decode_steps
+    M, b, H, d, L = w.layers, w.batch, w.heads, w.d_head, w.seq_len
+    theta = w.rope_theta
+    spans_all = W_.workload_spans(w)
+    Wr = max(kept_rows(s, L) for s in spans_all) + steps
+    L_cap = Wr + 1
+    dt = W_.torch_dtype(w.dtype)
+    meta = P.SpanMeta([[] for _ in range(b)], L + steps, dev)
+    cache = P.KVCache(M, b, H, L_cap, d, dt, dev)
+    ws = P.Workspace(b, H, 1, L_cap, d, dev)
+    for m in range(M):
+        for i, kv in enumerate((cache.k(m), cache.v(m))):
+            x = W_.randn((b, H, L, d), seed=w.seed * 100000 + m * 10 + 1 + i, dtype=w.dtype,
+                         device=dev)
+            P.ring_fill(x, kv, Wr, L, meta, theta if i == 0 else 0.0, L_cap)
+            del x
+    q_dec = W_.randn((steps, M, b, H, d), seed=w.seed * 100000 + 7001, dtype=w.dtype, device=dev)
+    k_dec = W_.randn((steps, M, b, H, d), seed=w.seed * 100000 + 7002, dtype=w.dtype, device=dev)
+    v_dec = W_.randn((steps, M, b, H, d), seed=w.seed * 100000 + 7003, dtype=w.dtype, device=dev)
+    od = torch.empty(b, H, d, dtype=dt, device=dev)
+    E = lambda: torch.cuda.Event(enable_timing=True)
+
+    def run(rec):
+        cache.cur_tok.fill_(L)
+        for t in range(steps):
+            if rec is not None:
+                rec[t][0].record()
+            for m in range(M):
+                P.local_decode_layer(q_dec[t, m], k_dec[t, m], v_dec[t, m], cache, m, Wr, meta, ws,
+                                     od, theta=theta)
+            if rec is not None:
+                rec[t][1].record()
+            cache.cur_tok.add_(1)
+
+    for _ in range(args.warmup):
+        run(None)
+    torch.cuda.synchronize()
+    recs = [[(E(), E()) for _ in range(steps)] for _ in range(args.steps)]
+    for r in recs:
+        run(r)
+    torch.cuda.synchronize()
+    if int(cache.status):
+        raise RuntimeError(f"device status {int(cache.status)}")
+    dec_ms = float(np.mean([sum(a.elapsed_time(z) for a, z in r) for r in recs]))
+    call_bytes = b * H * Wr * d * 2 * 2 + 6 * b * H * d * 2
+    gbs = M * steps * call_bytes / (dec_ms * 1e-3) / 1e9
+    out = {"metric": "local-attention comparator: decode over a ring of the W most recent tokens",
+           "value": round(gbs, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "higher_is_better": True, "vs_baseline": None,
+           "dtype": w.dtype, "data": "synthetic",
+           "config": {"workload": f"{w.name} shape, local attention at equal KV budget",
+                      "layers": M, "batch": b, "heads": H, "d_head": d, "prompt": L,
+                      "decode_steps": steps, "ring_rows": Wr, "rope_theta": theta},
+           "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
+                        "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+                        "avg_launch_us": round(dec_ms * 1e3 / (M * steps), 2),
+                        "bytes_per_launch": call_bytes},
+           "decode_tokens_per_s": round(b * steps / (dec_ms * 1e-3), 1),
+           "kv_bytes": int(M * 2 * b * H * Wr * d * (2 if w.dtype == "bf16" else 4))}
+    print(json.dumps(out), flush=True)
 
 
 def run_span_sweep(args, w):

@@ -254,6 +254,25 @@ int compacted_decode_attn(const void* q, const void* k_new, const void* v_new, v
                           int32_t* status, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
+ * Local-attention comparator (the "Local Attention" baseline of Section 4.1:
+ * a token attends only to a window of the most recent tokens), at a fixed
+ * budget of W cached rows: rows [0, W) of each slice are a ring holding the
+ * W most recent tokens, token t at row t mod W.  For each sequence with
+ * current token t = cur_tok[s], the new key (rotated at pos[s][t] when
+ * rope_theta > 0) and value replace row t mod W (the token t - W) and
+ * o[s,h] = attention of q over the W tokens t-W+1 .. t.  cur_tok is not
+ * changed.  A <CL> step (vu[s][t] == t) outputs v_new and writes nothing.
+ * Same launch shapes and workspace as compacted_decode_attn; bf16 only;
+ * 0 < W < L_cap.
+ * ------------------------------------------------------------------------- */
+int local_decode_attn(const void* q, const void* k_new, const void* v_new, void* k_cache,
+                      void* v_cache, int32_t W, const int32_t* cur_tok, const int32_t* vu,
+                      const int32_t* pos, int32_t L_meta, void* o, int32_t b, int32_t H,
+                      int32_t L_cap, int32_t d_head, sckv_dtype dt, float scale,
+                      float rope_theta, void* ws, size_t ws_bytes, int32_t* status,
+                      hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
  * Close a decode step after all layers: for each sequence, unless its current
  * token t = cur_tok[s] is a <CL> (vu[s][t] == t), record row kv_len[s]
  * (tok_idx = t, pos_ids = pos[s][t]) and increment kv_len[s]; then increment

@@ -69,6 +69,9 @@ _SIGS = {
                                              _i32, _i32, _i32, ctypes.c_int, _f32, _f32, _p, _sz,
                                              _p, _p]),
     "kv_commit": (ctypes.c_int, [_p, _p, _p, _p, _p, _p, _i32, _i32, _i32, _p, _p]),
+    "local_decode_attn": (ctypes.c_int, [_p, _p, _p, _p, _p, _i32, _p, _p, _p, _i32, _p, _i32,
+                                         _i32, _i32, _i32, ctypes.c_int, _f32, _f32, _p, _sz, _p,
+                                         _p]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _f = getattr(lib, _name)
@@ -211,3 +214,12 @@ def kv_commit(kv_len, tok_idx, pos_ids, cur_tok, vu, pos, L_meta: int, b: int, L
               status=None, stream=None):
     _check(lib.kv_commit(_ptr(kv_len), _ptr(tok_idx), _ptr(pos_ids), _ptr(cur_tok), _ptr(vu),
                          _ptr(pos), L_meta, b, L_cap, _ptr(status), _stream(stream, kv_len)))
+
+
+def local_decode_attn(q, k_new, v_new, k_cache, v_cache, W: int, cur_tok, vu, pos, L_meta: int,
+                      o, b: int, H: int, L_cap: int, d_head: int, scale: float, rope_theta: float,
+                      ws, status=None, stream=None):
+    _check(lib.local_decode_attn(_ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache),
+                                 W, _ptr(cur_tok), _ptr(vu), _ptr(pos), L_meta, _ptr(o), b, H,
+                                 L_cap, d_head, _dtype_code(q), scale, rope_theta, _ptr(ws),
+                                 ws.numel() * ws.element_size(), _ptr(status), _stream(stream, q)))

@@ -318,16 +318,22 @@ __global__ __launch_bounds__(64) void decode_combine_kernel(
     const T* __restrict__ v_new, const int32_t* __restrict__ kv_len,
     const int32_t* __restrict__ cur_tok, const int32_t* __restrict__ vu, int32_t L_meta,
     int32_t H, int32_t L_cap, const float* __restrict__ part, int32_t n_chunk_max, int32_t ch,
-    T* __restrict__ o, int32_t* __restrict__ status) {
+    T* __restrict__ o, int32_t* __restrict__ status, int32_t ring) {
   const int bh = blockIdx.x;
   const int s = bh / H;
   const int lane = threadIdx.x;
-  const int kind = step_kind(cur_tok, vu, kv_len, s, L_meta, L_cap);
+  int kind;
+  if (ring > 0) {  // the ring is always full: only token range and <CL> steps
+    const int t = cur_tok[s];
+    kind = (t < 0 || t >= L_meta) ? 2 : (vu[(int64_t)s * L_meta + t] == t ? 1 : 0);
+  } else {
+    kind = step_kind(cur_tok, vu, kv_len, s, L_meta, L_cap);
+  }
   if (kind != 0) {
     write_special<T, D>(kind, v_new, o, status, bh, H, lane, 64);
     return;
   }
-  const int nch = chunk_plan(kv_len[s] + 1, ch).n;
+  const int nch = chunk_plan((ring > 0 ? ring : kv_len[s]) + 1, ch).n;
   const float* p = part + (int64_t)bh * n_chunk_max * (D + 2);
   constexpr int PER = (D + 63) / 64;  // output elements per lane
   float M = -INFINITY, lsum = 0.f, acc[PER];
@@ -448,7 +454,7 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
     const int32_t* __restrict__ cur_tok, const int32_t* __restrict__ vu,
     const int32_t* __restrict__ pos, int32_t L_meta, int32_t H, int32_t L_cap, float qscale,
     int rotate, RopeTab tab, float* __restrict__ part, int32_t n_chunk_max, int32_t n_work,
-    int32_t ch, uint16_t* __restrict__ o, int32_t* __restrict__ status) {
+    int32_t ch, uint16_t* __restrict__ o, int32_t* __restrict__ status, int32_t ring) {
   constexpr int KS = D / 16;     // k steps of 16 elements
   constexpr int NA = 8 * KS;     // value elements per lane
   constexpr int THREADS = NW * 64;
@@ -470,7 +476,10 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
   // length is known and arrive while q is prepared.  The block addresses use
   // the length clamped into the cache, so they are valid whatever the step
   // turns out to be.
-  const int n_raw = kv_len[s];
+  // ring > 0 (local-attention comparator): rows [0, ring) are a ring of the
+  // ring most recent tokens, token t at row t mod ring; the new token
+  // replaces the oldest, whose row is not attended
+  const int n_raw = ring > 0 ? ring : kv_len[s];
   const int t_raw = cur_tok[s];
   const uint32_t* qw = reinterpret_cast<const uint32_t*>(q + (int64_t)bh * D);
   uint32_t qword[HD];
@@ -480,7 +489,8 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
   const int vu_t = t_ok ? vu[(int64_t)s * L_meta + t_raw] : 0;
   const int pos_t = (rotate && t_ok) ? pos[(int64_t)s * L_meta + t_raw] : 0;
 
-  const int n = min(max(n_raw, 0), L_cap - 1);
+  const int n = ring > 0 ? ring : min(max(n_raw, 0), L_cap - 1);
+  const int slot = (ring > 0 && t_ok) ? t_raw % ring : -1;  // row of the new token (ring)
   const int rows = n + 1;
   const ChunkPlan cp = chunk_plan(rows, ch);
   const int r0 = chunk * cp.rows;
@@ -506,7 +516,8 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
   if (wave + NW < nblk) load_blk(wave + NW, kB, vB);
 
   // the step kind, with the precedence of step_kind()
-  const int kind = !t_ok ? 2 : (vu_t == t_raw ? 1 : ((n_raw < 0 || n_raw >= L_cap) ? 3 : 0));
+  const int kind = !t_ok ? 2
+                   : (vu_t == t_raw ? 1 : ((ring == 0 && (n_raw < 0 || n_raw >= L_cap)) ? 3 : 0));
   if (kind != 0) {
     if constexpr (FINAL) write_special<uint16_t, D>(kind, v_new, o, status, bh, H, tid, THREADS);
     return;
@@ -586,7 +597,8 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
       c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qhi[kk], kv, c, 0, 0, 0);
       c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qlo[kk], kv, c, 0, 0, 0);
     }
-    const float sc = (r0 + 32 * i + kr < rc) ? c[0] * qscale : -INFINITY;
+    const int row = r0 + 32 * i + kr;
+    const float sc = (row < rc && row != slot) ? c[0] * qscale : -INFINITY;
     const float p = weigh(sc);
     if (h == 0) l += p;
 #pragma unroll
@@ -646,8 +658,9 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
     for (int u = 0; u < 2; ++u) {
       const int t = lane + 64 * u;
       if (t < D) {
-        k_cache[((int64_t)bh * L_cap + n) * D + t] = kq[u];
-        v_cache[((int64_t)bh * L_cap + n) * D + t] = vx[t];
+        const int64_t dst = (int64_t)bh * L_cap + (ring > 0 ? slot : n);
+        k_cache[dst * D + t] = kq[u];
+        v_cache[dst * D + t] = vx[t];
       }
     }
   }
@@ -706,7 +719,7 @@ static int launch_decode(const void* q, const void* k_new, const void* v_new, vo
                          void* v_cache, const int32_t* kv_len, const int32_t* cur_tok,
                          const int32_t* vu, const int32_t* pos, int32_t L_meta, void* o,
                          int32_t b, int32_t H, int32_t L_cap, float scale, float theta,
-                         void* ws, int32_t* status, hipStream_t stream) {
+                         void* ws, int32_t* status, hipStream_t stream, int32_t ring = 0) {
   RopeTab tab;
   for (int i = 0; i < 40; ++i) tab.w[i] = 0.0;
   const int rotate = theta > 0.f ? 1 : 0;
@@ -727,11 +740,11 @@ static int launch_decode(const void* q, const void* k_new, const void* v_new, vo
       if (narrow)
         decode_mfma_kernel<D, 2, true><<<slices, 128, 0, stream>>>(
             qq, kn, vn, kc, vc, kv_len, cur_tok, vu, pos, L_meta, H, L_cap, qs, rotate, tab, part,
-            1, slices, L_cap, out, status);
+            1, slices, L_cap, out, status, ring);
       else
         decode_mfma_kernel<D, 4, true><<<slices, 256, 0, stream>>>(
             qq, kn, vn, kc, vc, kv_len, cur_tok, vu, pos, L_meta, H, L_cap, qs, rotate, tab, part,
-            1, slices, L_cap, out, status);
+            1, slices, L_cap, out, status, ring);
     } else {
       if (narrow)
         decode_chunk_kernel<T, D, 256, true><<<slices, 256, 0, stream>>>(
@@ -749,7 +762,7 @@ static int launch_decode(const void* q, const void* k_new, const void* v_new, vo
   if constexpr (sizeof(T) == 2)
     decode_mfma_kernel<D, 4, false><<<n_work, 256, 0, stream>>>(
         qq, kn, vn, kc, vc, kv_len, cur_tok, vu, pos, L_meta, H, L_cap, qs, rotate, tab, part, nc,
-        n_work, DEC_CH, out, status);
+        n_work, DEC_CH, out, status, ring);
   else
     decode_chunk_kernel<T, D, DEC_THREADS, false><<<n_work, DEC_THREADS, 0, stream>>>(
         qq, kn, vn, kc, vc, kv_len, cur_tok, vu, pos, L_meta, H, L_cap, qs, rotate, tab, part, nc,
@@ -757,7 +770,7 @@ static int launch_decode(const void* q, const void* k_new, const void* v_new, vo
   int rc = hip_check(hipGetLastError(), "compacted_decode_attn: chunk launch");
   if (rc) return rc;
   decode_combine_kernel<T, D><<<slices, 64, 0, stream>>>(vn, kv_len, cur_tok, vu, L_meta, H, L_cap,
-                                                          part, nc, DEC_CH, out, status);
+                                                          part, nc, DEC_CH, out, status, ring);
   return hip_check(hipGetLastError(), "compacted_decode_attn: combine launch");
 }
 
@@ -768,6 +781,38 @@ using namespace sckv;
 extern "C" size_t sckv_decode_workspace_bytes(int32_t b, int32_t H, int32_t L_cap, int32_t d_head) {
   if (b <= 0 || H <= 0 || L_cap <= 0 || d_head <= 0) return 0;
   return (size_t)b * H * n_chunks(L_cap) * (d_head + 2) * sizeof(float);
+}
+
+extern "C" int local_decode_attn(const void* q, const void* k_new, const void* v_new,
+                                 void* k_cache, void* v_cache, int32_t W, const int32_t* cur_tok,
+                                 const int32_t* vu, const int32_t* pos, int32_t L_meta, void* o,
+                                 int32_t b, int32_t H, int32_t L_cap, int32_t d_head,
+                                 sckv_dtype dt, float scale, float rope_theta, void* ws,
+                                 size_t ws_bytes, int32_t* status, hipStream_t stream) {
+  clear_error();
+  if (!q || !k_new || !v_new || !k_cache || !v_cache || !cur_tok || !vu || !o || !ws)
+    return fail(SCKV_EINVAL, "local_decode_attn: null pointer");
+  if (dt != SCKV_BF16) return fail(SCKV_EUNSUP, "local_decode_attn: bf16 only");
+  if (!supported_d(d_head)) return fail(SCKV_EUNSUP, "local_decode_attn: d_head must be 64 or 80");
+  // W < L_cap: the W ring rows and the new token make W + 1 <= L_cap rows of
+  // work, the most the launch and the workspace are sized for
+  if (b <= 0 || H <= 0 || L_cap <= 0 || L_meta <= 0 || W <= 0 || W >= L_cap)
+    return fail(SCKV_EINVAL, "local_decode_attn: need 0 < W < L_cap and positive sizes");
+  if ((int64_t)b * H * n_chunks(L_cap) > 0x7fffffff)
+    return fail(SCKV_EUNSUP, "local_decode_attn: b*H*chunks too large");
+  if (!(scale > 0.f) || std::isinf(scale)) return fail(SCKV_EINVAL, "local_decode_attn: scale must be finite and > 0");
+  if (!(rope_theta >= 0.f) || std::isinf(rope_theta))
+    return fail(SCKV_EINVAL, "local_decode_attn: rope_theta must be finite and >= 0");
+  if (rope_theta > 0.f && !pos) return fail(SCKV_EINVAL, "local_decode_attn: null pos");
+  if (ws_bytes < sckv_decode_workspace_bytes(b, H, L_cap, d_head))
+    return fail(SCKV_EINVAL, "local_decode_attn: workspace too small");
+  if (!aligned16(q) || !aligned16(k_new) || !aligned16(v_new) || !aligned16(k_cache) ||
+      !aligned16(v_cache) || !aligned16(o) || !aligned16(ws))
+    return fail(SCKV_EINVAL, "local_decode_attn: buffers must be 16-byte aligned");
+  const int32_t* p = pos ? pos : vu;
+  return d_head == 64
+             ? launch_decode<uint16_t, 64>(q, k_new, v_new, k_cache, v_cache, nullptr, cur_tok, vu, p, L_meta, o, b, H, L_cap, scale, rope_theta, ws, status, stream, W)
+             : launch_decode<uint16_t, 80>(q, k_new, v_new, k_cache, v_cache, nullptr, cur_tok, vu, p, L_meta, o, b, H, L_cap, scale, rope_theta, ws, status, stream, W);
 }
 
 extern "C" int compacted_decode_attn(const void* q, const void* k_new, const void* v_new,

@@ -173,3 +173,34 @@ def prefill_progressive(q, k, v, o, cache: KVCache, meta: SpanMeta, ws: Workspac
         if on_block is not None:
             on_block(B0 + n)
     cache.cur_tok.fill_(L)
+
+
+# ---------------------------------------------------------------------------
+# local-attention comparator: a ring of the W most recent tokens
+# ---------------------------------------------------------------------------
+
+def ring_fill(x, y, W: int, L: int, meta: SpanMeta, theta: float, L_cap: int, stream=None):
+    """Rotate tokens [L-W, L) of x (b, H, >=L, d) into the ring slices y
+    (b, H, L_cap, d), token t at row t mod W."""
+    b, H, _, d = x.shape
+    t0 = L - W
+    a = t0 % W
+    pieces = ((t0, t0 + (W - a), a), (t0 + (W - a), L, 0))  # (first token, end, first row)
+    for ts, te, r in pieces:
+        if te <= ts:
+            continue
+        row0 = torch.full((b,), r, dtype=torch.int32, device=x.device)
+        xs = x[:, :, ts:te]
+        B.rope_apply_at(xs, y, row0, L_cap, b, H, te - ts, xs.stride(1), y.stride(1), d, meta.pos,
+                        meta.L_meta, ts, theta, stream=stream)
+
+
+def local_decode_layer(q, k_new, v_new, cache: KVCache, m: int, W: int, meta: SpanMeta,
+                       ws: Workspace, o, scale=None, theta: float = 0.0, stream=None):
+    """Attention of the current token over the W most recent tokens held in
+    the ring rows of layer m; the new token replaces the oldest."""
+    d = q.shape[-1]
+    B.local_decode_attn(q, k_new, v_new, cache.k(m), cache.v(m), W, cache.cur_tok, meta.vu,
+                        meta.pos, meta.L_meta, o, cache.b, cache.H, cache.L_cap, d,
+                        default_scale(d) if scale is None else scale, theta, ws.decode,
+                        cache.status, stream=stream)

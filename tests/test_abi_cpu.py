@@ -178,3 +178,21 @@ def test_block_entry_points_reject_bad_arguments(B):
     assert call(ws=ws - 1) == B.EINVAL
     assert call(d=96) == B.EUNSUP
     assert call(scale=0.0) == B.EINVAL
+
+
+def test_local_decode_rejects_bad_arguments(B):
+    lib = B.lib
+    ws = lib.sckv_decode_workspace_bytes(2, 4, 64, 80)
+
+    def call(**kw):
+        a = dict(W=32, L_cap=64, dt=B.BF16, d=80, ws=ws, cur=FAKE)
+        a.update(kw)
+        return lib.local_decode_attn(FAKE, FAKE, FAKE, FAKE, FAKE, a["W"], a["cur"], FAKE, FAKE,
+                                     100, FAKE, 2, 4, a["L_cap"], a["d"], a["dt"], 0.1, 0.0, FAKE,
+                                     a["ws"], NULL, NULL)
+    assert call(W=64) == B.EINVAL        # W must be below L_cap
+    assert call(W=0) == B.EINVAL
+    assert call(dt=B.F32) == B.EUNSUP     # bf16 only
+    assert call(d=72) == B.EUNSUP
+    assert call(ws=ws - 4) == B.EINVAL
+    assert call(cur=NULL) == B.EINVAL

@@ -483,3 +483,58 @@ def test_end_to_end_prompt_compact_decode(case):
             assert int(cache.kv_len[s]) == fin[4]
             assert np.array_equal(cache.tok_idx[s, :fin[4]].cpu().numpy(), fin[2][:fin[4]])
             assert np.array_equal(cache.pos_ids[s, :fin[4]].cpu().numpy(), fin[3][:fin[4]])
+
+
+# ---------------------------------------------------------------------------
+# local-attention comparator: ring of the W most recent tokens
+# ---------------------------------------------------------------------------
+
+# H=3 splits each slice into chunks (merge kernel); H=256 with b=2 gives 512
+# slices, one workgroup each
+@pytest.mark.parametrize("d,theta,H,W", [(80, 10000.0, 3, 50), (64, 0.0, 3, 37),
+                                         (80, 10000.0, 256, 50)])
+def test_local_decode_ring_matches_oracle(d, theta, H, W):
+    say(f"local decode d={d} theta={theta} H={H} W={W}")
+    b, L, steps = 2, 120, 70  # 70 steps wrap the ring more than once
+    T = L + steps
+    meta = P().SpanMeta([[] for _ in range(b)], T, DEV)
+    L_cap = W + 3
+    cache = P().KVCache(1, b, H, L_cap, d, torch.bfloat16, DEV)
+    ws = P().Workspace(b, H, 1, L_cap, d, DEV)
+    k0, v0 = (rnd((b, H, L, d), 900 + i, "bf16") for i in range(2))
+    P().ring_fill(k0, cache.k(0), W, L, meta, theta, L_cap)
+    P().ring_fill(v0, cache.v(0), W, L, meta, 0.0, L_cap)
+    cache.cur_tok.fill_(L)
+    qd, kd, vd = (rnd((steps, b, H, d), 910 + i, "bf16") for i in range(3))
+    od = torch.empty(b, H, d, dtype=torch.bfloat16, device=DEV)
+    got = []
+    for i in range(steps):
+        P().local_decode_layer(qd[i], kd[i], vd[i], cache, 0, W, meta, ws, od, theta=theta)
+        got.append(f64(od))
+        cache.cur_tok.add_(1)
+    torch.cuda.synchronize()
+    assert int(cache.status) == 0
+    # oracle: keys of all tokens rotated at their positions (no sentinels:
+    # position = index), attention over the last W tokens
+    K = np.concatenate([f64(k0), np.transpose(f64(kd), (1, 2, 0, 3))], axis=2)
+    V = np.concatenate([f64(v0), np.transpose(f64(vd), (1, 2, 0, 3))], axis=2)
+    Q = f64(qd)
+    worst = 0.0
+    for s in range(b):
+        for h in range(H):
+            Kr = O.rope_rotate_half(K[s, h], np.arange(T), theta) if theta > 0 else K[s, h]
+            Kr = f64(torch.tensor(Kr).to(torch.bfloat16))  # the cache stores rotated keys in bf16
+            for i in range(steps):
+                t = L + i
+                qs = Q[i, s, h][None]
+                if theta > 0:
+                    qs = O.rope_rotate_half(qs, [t], theta)
+                lo = t - W + 1
+                ref = O.decode_attention(qs, Kr[t][None], V[s, h, t][None], Kr[lo:t][None],
+                                         V[s, h, lo:t][None], W - 1, False)[0]
+                worst = max(worst, np.abs(got[i][s, h] - ref).max())
+    assert worst <= TOL["bf16"], worst
+    # the ring holds the last W tokens, token t at row t mod W
+    Kc, Vc = f64(cache.k(0)), f64(cache.v(0))
+    for t in range(T - W, T):
+        assert np.array_equal(Vc[:, :, t % W], V[:, :, t])
