@@ -328,30 +328,53 @@ __device__ __forceinline__ void prefill_attn_body(
   // first, then the copies are issued.  The indices come from row_ring, which
   // holds them bare: no masking of the packed entry happens on this path.
   constexpr int KRND = (TL::KSLOT + 3) / 4, VRND = (TL::VSLOT + 3) / 4;
+  // Copies go through buffer loads with an LDS destination: a 32-bit byte
+  // offset per lane against a descriptor of the slice (reads past the slice
+  // return zeros instead of faulting), the LDS block address in scalar
+  // registers.  Each lane's tile row and piece offset per round are fixed
+  // for the kernel and computed once here.
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+  const int slice_bytes = (int)min((int64_t)kvs * (int64_t)sizeof(T), (int64_t)0x7fffffff);
+  const __amdgpu_buffer_rsrc_t krs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(kb), 0, slice_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t vrs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(vb), 0, slice_bytes, 0x00020000);
+  constexpr int ROWB = D * (int)sizeof(T);
+  int k_row[KRND], k_off[KRND], v_row[VRND], v_off[VRND];
+#pragma unroll
+  for (int rnd = 0; rnd < KRND; ++rnd) {
+    const int sl = (rnd * 4 + wave) * 64 + lane;
+    const int sg = sl % TL::KSLOT;
+    k_row[rnd] = min(sl / TL::KSLOT, PF_BK - 1);
+    k_off[rnd] = sg < TL::PPR ? sg * 16 : -1;
+  }
+#pragma unroll
+  for (int rnd = 0; rnd < VRND; ++rnd) {
+    const int sl = (rnd * 4 + wave) * 64 + lane;
+    const int sg = sl % TL::VSLOT;
+    v_row[rnd] = min(sl / TL::VSLOT, PF_BK - 1);
+    v_off[rnd] = sg < TL::PPR ? sg * 16 : -1;
+  }
   auto dma_rows = [&](int kt, char* kdst, char* vdst) {
     const int32_t* rows = row_ring[kt % PF_ER];
     int kj[KRND], vj[VRND];
 #pragma unroll
-    for (int rnd = 0; rnd < KRND; ++rnd)
-      kj[rnd] = rows[min(((rnd * 4 + wave) * 64 + lane) / TL::KSLOT, PF_BK - 1)];
+    for (int rnd = 0; rnd < KRND; ++rnd) kj[rnd] = rows[k_row[rnd]];
 #pragma unroll
-    for (int rnd = 0; rnd < VRND; ++rnd)
-      vj[rnd] = rows[min(((rnd * 4 + wave) * 64 + lane) / TL::VSLOT, PF_BK - 1)];
+    for (int rnd = 0; rnd < VRND; ++rnd) vj[rnd] = rows[v_row[rnd]];
 #pragma unroll
     for (int rnd = 0; rnd < KRND; ++rnd) {
-      const int blk = rnd * 4 + wave;
-      const int sg = (blk * 64 + lane) % TL::KSLOT;
-      if (blk < TL::KSLOT && sg < TL::PPR)
-        __builtin_amdgcn_global_load_lds(kb + (int64_t)kj[rnd] * D + sg * C::E,
-                                         (lds_ptr_t)(kdst + blk * 1024), 16, 0, 0);
+      const int blk = rnd * 4 + wave_s;
+      if (blk < TL::KSLOT && k_off[rnd] >= 0)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(krs, (lds_ptr_t)(kdst + blk * 1024), 16,
+                                                 kj[rnd] * ROWB + k_off[rnd], 0, 0, 0);
     }
 #pragma unroll
     for (int rnd = 0; rnd < VRND; ++rnd) {
-      const int blk = rnd * 4 + wave;
-      const int sg = (blk * 64 + lane) % TL::VSLOT;
-      if (blk < TL::VSLOT && sg < TL::PPR)
-        __builtin_amdgcn_global_load_lds(vb + (int64_t)vj[rnd] * D + sg * C::E,
-                                         (lds_ptr_t)(vdst + blk * 1024), 16, 0, 0);
+      const int blk = rnd * 4 + wave_s;
+      if (blk < TL::VSLOT && v_off[rnd] >= 0)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(vrs, (lds_ptr_t)(vdst + blk * 1024), 16,
+                                                 vj[rnd] * ROWB + v_off[rnd], 0, 0, 0);
     }
   };
 
