@@ -397,23 +397,6 @@ __global__ __launch_bounds__(64) void decode_combine_kernel(
 // rows are in flight while a block is computed.
 constexpr float DM_RESCALE = 8.f;
 
-template <int D>
-__device__ __forceinline__ float rot_elem(const uint16_t* x, int t, bool rotate, double ps,
-                                          const double* inv) {
-  const float xv = bf16_lo((uint32_t)x[t]);
-  if (!rotate) return xv;
-  constexpr int HD = D / 2;
-  const bool first = t < HD;
-  const float pv = bf16_lo((uint32_t)x[first ? t + HD : t - HD]);
-  const double two_pi = 6.283185307179586476925286766559;
-  const double inv_two_pi = 0.15915494309189533576888376337251;
-  double ang = ps * inv[first ? t : t - HD];
-  ang -= two_pi * rint(ang * inv_two_pi);
-  float sn, cs;
-  sincosf((float)ang, &sn, &cs);
-  return first ? xv * cs - pv * sn : xv * cs + pv * sn;
-}
-
 // Sums v[0..NV) over the 32 lanes of each half-wave.  While NV is even a
 // step halves the values a lane keeps (the lane whose MASK bit is set keeps
 // the upper half); odd counts finish with plain butterflies.  On return the
@@ -459,6 +442,7 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
   constexpr int NA = 8 * KS;     // value elements per lane
   constexpr int THREADS = NW * 64;
   constexpr int HD = D / 2;
+  static_assert(D >= 64 && D <= 128 && D % 16 == 0, "one or two elements per lane of wave 0");
   // chunk-major order (as in decode_chunk_kernel)
   const int n_bh = n_work / n_chunk_max;
   const int chunk = blockIdx.x / n_bh;
@@ -481,6 +465,16 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
   // replaces the oldest, whose row is not attended
   const int n_raw = ring > 0 ? ring : kv_len[s];
   const int t_raw = cur_tok[s];
+  // the new row: thread tid < D takes element tid of k_new and v_new and
+  // the element k_new rotates against.  These vector loads go out before the
+  // block loads (the counter retires in issue order), so the new row is
+  // ready before the first block and its latency hides under the stream.
+  // Threads past D re-read element D - 1.
+  const int te = min(tid, D - 1);
+  const int tp = te < HD ? te + HD : te - HD;
+  const uint16_t kx_raw = k_new[(int64_t)bh * D + te];
+  const uint16_t kp_raw = k_new[(int64_t)bh * D + tp];
+  const uint16_t vx_raw = v_new[(int64_t)bh * D + te];
   const uint32_t* qw = reinterpret_cast<const uint32_t*>(q + (int64_t)bh * D);
   uint32_t qword[HD];
 #pragma unroll
@@ -497,13 +491,14 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
   const int r1 = min(r0 + cp.rows, rows);
   const int rc = min(r1, n);  // cache rows of this chunk: [r0, rc)
   const int nblk = chunk < cp.n ? (rc - r0 + 31) / 32 : 0;
+  const bool holds_new = n >= r0 && n < r1;
 
   const uint16_t* kb = k_cache + (int64_t)bh * L_cap * D;
   const uint16_t* vb = v_cache + (int64_t)bh * L_cap * D;
-  // rows past rc re-read row rc-1 (always present when a block exists);
+  // rows past rc re-read row rc-1 (row 0 where the chunk has no rows);
   // their scores are masked
   auto load_blk = [&](int i, u32x4* kd, u32x4* vd) {
-    const int row = min(r0 + 32 * i + kr, rc - 1);
+    const int row = max(min(r0 + 32 * i + kr, rc - 1), 0);
     const uint16_t* kp = kb + (int64_t)row * D + 8 * h;
     const uint16_t* vp = vb + (int64_t)row * D + 8 * h;
 #pragma unroll
@@ -511,9 +506,11 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk) vd[kk] = ld16(vp + 16 * kk);
   };
+  // issued whether or not the wave has these blocks, so that the counter
+  // waits below stay exact on every path
   u32x4 kA[KS], vA[KS], kB[KS], vB[KS];
-  if (wave < nblk) load_blk(wave, kA, vA);
-  if (wave + NW < nblk) load_blk(wave + NW, kB, vB);
+  load_blk(wave, kA, vA);
+  load_blk(wave + NW, kB, vB);
 
   // the step kind, with the precedence of step_kind()
   const int kind = !t_ok ? 2
@@ -524,12 +521,11 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
   }
   if (chunk >= cp.n) return;
 
-  // rotated q element tid (tid < D) from the words held in scalar registers;
-  // the frequencies go to LDS for the new key
-  __shared__ float qs[D];
-  __shared__ double inv[HD];
+  // rotated q and k elements tid (tid < D), q from the words held in scalar
+  // registers; both turn by the same angle.  The key is rounded to bf16 as
+  // stored; its product with q and the value element go to LDS.
+  __shared__ float qs[D], kqs[D], vs[D];
   if (tid < D) {
-    const int tp = tid < HD ? tid + HD : tid - HD;
     uint32_t xw = 0, pw = 0;
 #pragma unroll
     for (int j = 0; j < HD; ++j) {
@@ -537,12 +533,13 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
       pw = (tp >> 1) == j ? qword[j] : pw;
     }
     float x = (tid & 1) ? bf16_hi(xw) : bf16_lo(xw);
+    float kx = bf16_lo((uint32_t)kx_raw);
     if (rotate) {
       const float pv = (tp & 1) ? bf16_hi(pw) : bf16_lo(pw);
+      const float kp = bf16_lo((uint32_t)kp_raw);
       double w = 0.0;
 #pragma unroll
       for (int j = 0; j < HD; ++j) w = (tid % HD) == j ? tab.w[j] : w;
-      if (tid < HD) inv[tid] = w;
       const double two_pi = 6.283185307179586476925286766559;
       const double inv_two_pi = 0.15915494309189533576888376337251;
       double ang = (double)pos_t * w;
@@ -550,8 +547,17 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
       float sn, cs;
       sincosf((float)ang, &sn, &cs);
       x = tid < HD ? x * cs - pv * sn : x * cs + pv * sn;
+      kx = tid < HD ? kx * cs - kp * sn : kx * cs + kp * sn;
     }
+    const uint16_t kq = f32_to_bf16(kx);
     qs[tid] = x;
+    kqs[tid] = x * bf16_lo((uint32_t)kq);
+    vs[tid] = bf16_lo((uint32_t)vx_raw);
+    if (holds_new) {
+      const int64_t dst = (int64_t)bh * L_cap + (ring > 0 ? slot : n);
+      k_cache[dst * D + tid] = kq;
+      v_cache[dst * D + tid] = vx_raw;
+    }
   }
   __syncthreads();
 
@@ -612,58 +618,43 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
     }
   };
 
-  // blocks wave, wave + NW are in flight; each computed buffer is refilled
-  // with the block 2 NW further on
-  for (int i = wave; i < nblk; i += 2 * NW) {
-    compute(i, kA, vA);
-    if (i + 2 * NW < nblk) load_blk(i + 2 * NW, kA, vA);
-    if (i + NW >= nblk) break;
-    compute(i + NW, kB, vB);
-    if (i + 3 * NW < nblk) load_blk(i + 3 * NW, kB, vB);
-  }
-
-  // the new row: rotated k_new (rounded to bf16 as stored) and v_new, taken
-  // in by wave 0 and written to the cache
-  if (n >= r0 && n < r1 && wave == 0) {
-    const uint16_t* kx = k_new + (int64_t)bh * D;
-    const uint16_t* vx = v_new + (int64_t)bh * D;
-    float prod = 0.f;
-    uint16_t kq[2] = {0, 0};
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int t = lane + 64 * u;
-      if (t < D) {
-        kq[u] = f32_to_bf16(rot_elem<D>(kx, t, rotate, (double)pos_t, inv));
-        prod = fmaf(qs[t], bf16_lo((uint32_t)kq[u]), prod);
-      }
-    }
+  // the new row opens the state of wave 0: its score is the sum of the
+  // products in LDS; lanes 0 and 32 take the value elements they own and
+  // lane 0 counts the weight
+  if (holds_new && wave == 0) {
+    float prod = kqs[lane];
+    if (lane + 64 < D) prod += kqs[lane + 64];
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) prod += __shfl_xor(prod, off, 64);
-    // every lane takes the score; lanes 0 and 32 add the value elements they
-    // own, lane 0 counts the weight
     const float p = weigh(prod * qscale);
     if (lane == 0) l += p;
     if (kr == 0) {
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) {
-        const u32x4 w = ld16(vx + 16 * kk + 8 * h);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          acc[8 * kk + 2 * j] = fmaf(p, bf16_lo(w[j]), acc[8 * kk + 2 * j]);
-          acc[8 * kk + 2 * j + 1] = fmaf(p, bf16_hi(w[j]), acc[8 * kk + 2 * j + 1]);
-        }
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int t = lane + 64 * u;
-      if (t < D) {
-        const int64_t dst = (int64_t)bh * L_cap + (ring > 0 ? slot : n);
-        k_cache[dst * D + t] = kq[u];
-        v_cache[dst * D + t] = vx[t];
+        for (int j = 0; j < 8; ++j) acc[8 * kk + j] = p * vs[16 * kk + 8 * h + j];
       }
     }
   }
+
+  // blocks wave, wave + NW are in flight; each computed buffer is refilled
+  // with the block 2 NW further on.  The steady state loads without a
+  // condition, so each buffer is written in place and the loop carries no
+  // register copies (a copy would have to wait for its load to land).
+  int i = wave;
+  for (; i + 3 * NW < nblk; i += 2 * NW) {
+    compute(i, kA, vA);
+    load_blk(i + 2 * NW, kA, vA);
+    compute(i + NW, kB, vB);
+    load_blk(i + 3 * NW, kB, vB);
+  }
+  // at most three blocks remain: i and i + NW in flight, i + 2 NW to load
+  if (i < nblk) {
+    compute(i, kA, vA);
+    if (i + 2 * NW < nblk) load_blk(i + 2 * NW, kA, vA);
+  }
+  if (i + NW < nblk) compute(i + NW, kB, vB);
+  if (i + 2 * NW < nblk) compute(i + 2 * NW, kA, vA);
 
   // wave partials: l over the wave, values over each half-wave
 #pragma unroll
