@@ -165,6 +165,15 @@ struct TileInfo {
   int jmin, jmax, vrmin, nvalid;
 };
 
+// maximum of x over lanes l and l^32: one lane swap between the two
+// 32-lane halves of the wave (v_permlane32_swap leaves each lane holding
+// the pair's two values, one in each result)
+__device__ __forceinline__ float max_across_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  const float a = __uint_as_float(r[0]), b = __uint_as_float(r[1]);
+  return a > b ? a : b;
+}
+
 constexpr int PF_ER = 4;  // ring of list entries: tile kt+2 is fetched while kt is computed
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
@@ -295,28 +304,41 @@ __device__ __forceinline__ void prefill_attn_body(
     ereg = in ? ents[kt * PF_BK + tid] : PF_NONE;
     if constexpr (CACHED) rreg = in ? (int)rws[kt * PF_BK + tid] : 0;
   };
+  // Wave 0 writes the ring slot of tile kt; every reduction over the tile
+  // stays in scalar registers (lane reads and ballots), with no cross-lane
+  // LDS traffic on the way to the barrier that ends the step.
   auto store_entries = [&](int kt) {
     const int slot = kt % PF_ER;
-    if (tid < 64) {
-      const int nvalid = nvalid_of(kt);
-      ent_ring[slot][tid] = ereg;
-      int vr = (tid < nvalid) ? (int)(ereg >> 24) : 255;
+    if (wave == 0) {
+      const int nvalid = nvalid_of(kt);  // >= 1: kt is a tile of the list
+      const int last = max(nvalid - 1, 0);
+      ent_ring[slot][lane] = ereg;
+      // smallest rank byte of the valid entries, from the top bit down: the
+      // candidates shrink to those with a 0 in the next bit whenever any has
+      const uint32_t vr = lane < nvalid ? (ereg >> 24) : 255u;
+      uint64_t cand = ~0ull;
+      int vrmin = 0;
 #pragma unroll
-      for (int off = 1; off < 64; off <<= 1) vr = min(vr, __shfl_xor(vr, off, 64));
-      const int jmax = __shfl((int)(ereg & 0x00ffffffu), nvalid - 1, 64);
+      for (int bit = 7; bit >= 0; --bit) {
+        const uint64_t z = __ballot(((vr >> bit) & 1u) == 0u) & cand;
+        if (z != 0) cand = z;
+        else vrmin |= 1 << bit;
+      }
+      const int jmin = __builtin_amdgcn_readlane((int)(ereg & 0x00ffffffu), 0);
+      const int jmax = __builtin_amdgcn_readlane((int)(ereg & 0x00ffffffu), last);
       // a padding row of the tile repeats the last valid row (its score is
       // masked, so any finite row will do)
       if constexpr (CACHED) {
-        const int rlast = __shfl(rreg, nvalid - 1, 64);
-        row_ring[slot][tid] = tid < nvalid ? rreg : rlast;
+        const int rlast = __builtin_amdgcn_readlane(rreg, last);
+        row_ring[slot][lane] = lane < nvalid ? rreg : rlast;
       } else {
-        row_ring[slot][tid] = tid < nvalid ? (int)(ereg & 0x00ffffffu) : jmax;
+        row_ring[slot][lane] = lane < nvalid ? (int)(ereg & 0x00ffffffu) : jmax;
       }
-      if (tid == 0) {
+      if (lane == 0) {
         TileInfo ti;
-        ti.jmin = (int)(ereg & 0x00ffffffu);
+        ti.jmin = jmin;
         ti.jmax = jmax;
-        ti.vrmin = vr;
+        ti.vrmin = vrmin;
         ti.nvalid = nvalid;
         info_ring[slot] = ti;
       }
@@ -424,7 +446,7 @@ __device__ __forceinline__ void prefill_attn_body(
       for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
         for (int vv = 0; vv < 16; ++vv) mx = fmaxf(mx, sacc[kb2][vv]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * c2;
+      mx = max_across_halves(mx) * c2;
       const bool grow = mx > m_run + PF_RESCALE;
       if (__ballot(grow) != 0) {
         const float alpha = grow ? fast_exp2(m_run - mx) : 1.f;  // m_run == -inf gives 0
