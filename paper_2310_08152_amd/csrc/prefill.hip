@@ -11,6 +11,9 @@
 //   row of the block may see, in ascending order, packed as
 //   j | min(vu[j]-I, 255) << 24.  Columns hidden from the whole block (closed
 //   spans, <CL>s before the block) are not in the list and are never read.
+//   It then summarises each 64-entry tile of the list (first and last token,
+//   smallest rank, valid entries), so the main kernel stages a tile without
+//   reductions of its own.
 // main kernel: one workgroup per (sequence, head, query block), 4 waves of 32
 //   query rows.  Key/value rows named by the list are gathered 64 at a time
 //   into LDS (double buffered for bf16); S^T = K Q^T and O^T += V^T P^T run
@@ -59,6 +62,13 @@ struct PfCached {
   int32_t* status;       // nullable: SCKV_STATUS_CAP for a block that does not fit
 };
 
+// Summary of one 64-entry tile of a list, written by the plan kernel: first
+// and last listed token, smallest rank byte | valid entries << 8, and the row
+// a padding slot of the tile repeats (the last valid entry's row).
+struct TileSum {
+  int32_t jmin, jmax, vr_n, pad_row;
+};
+
 // Plain: columns j < min(I+128, L) with token j.  Cached: cache rows
 // r < row0 + min(I_loc+128, nq) with token tok[r], where I_loc is the query
 // block's first local row and I = tok0 + I_loc its first token.
@@ -68,6 +78,7 @@ __global__ __launch_bounds__(256) void prefill_plan_kernel(const int32_t* __rest
                                                            int32_t L_pad,
                                                            uint32_t* __restrict__ list,
                                                            int32_t* __restrict__ count,
+                                                           TileSum* __restrict__ info,
                                                            PfCached cc) {
   const int qt = blockIdx.x;
   const int s = blockIdx.y;
@@ -118,6 +129,26 @@ __global__ __launch_bounds__(256) void prefill_plan_kernel(const int32_t* __rest
     __syncthreads();
   }
   if (tid == 0) count[(int64_t)s * n_qt + qt] = carry;
+
+  // tile summaries: wave w takes tiles w, w+4, ... of the list just written
+  // (the barrier that ended the last round orders those writes before these
+  // reads)
+  const int lane = tid & 63;
+  const uint32_t* rws = CACHED ? cc.rows + ((int64_t)s * n_qt + qt) * L_pad : nullptr;
+  TileSum* sum = info + ((int64_t)s * n_qt + qt) * (L_pad / 64);
+  for (int t = wave; t * 64 < carry; t += 4) {
+    const int nvalid = min(64, carry - t * 64);
+    const bool in = lane < nvalid;
+    const uint32_t e = in ? out[t * 64 + lane] : PF_NONE;
+    int vr = in ? (int)(e >> 24) : 255;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) vr = min(vr, __shfl_xor(vr, off, 64));
+    const int jmin = __shfl((int)(e & 0x00ffffffu), 0, 64);
+    const int jmax = __shfl((int)(e & 0x00ffffffu), nvalid - 1, 64);
+    int pad = jmax;
+    if constexpr (CACHED) pad = __shfl(in ? (int)rws[t * 64 + lane] : 0, nvalid - 1, 64);
+    if (lane == 0) sum[t] = TileSum{jmin, jmax, vr | (nvalid << 8), pad};
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -186,8 +217,8 @@ __device__ __forceinline__ void prefill_attn_body(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v, T* __restrict__ o,
     int32_t H, int32_t L, int64_t qs, int64_t kvs, int64_t os, float c2,
     const int32_t* __restrict__ vu, int32_t L_meta, const uint32_t* __restrict__ list,
-    const int32_t* __restrict__ count, int32_t n_qt, int32_t L_pad, int32_t n_work,
-    PfCached cc) {
+    const int32_t* __restrict__ count, const TileSum* __restrict__ info, int32_t n_qt,
+    int32_t L_pad, int32_t n_work, PfCached cc) {
   using C = PfCfg<T, D>;
   using TL = PfTile<T, D>;
   constexpr bool BF = sizeof(T) == 2;
@@ -233,6 +264,7 @@ __device__ __forceinline__ void prefill_attn_body(
   const T* vb = v + (int64_t)bh * kvs;
   const uint32_t* ents = list + ((int64_t)s * n_qt + qt) * L_pad;
   const uint32_t* rws = CACHED ? cc.rows + ((int64_t)s * n_qt + qt) * L_pad : nullptr;
+  const TileSum* tsum = info + ((int64_t)s * n_qt + qt) * (L_pad / 64);
   int own_row0 = 0;  // cache row of local query row 0
   if constexpr (CACHED) {
     own_row0 = cc.row0[s];
@@ -298,47 +330,31 @@ __device__ __forceinline__ void prefill_attn_body(
   // from the ring while tile kt is multiplied ----
   uint32_t ereg = PF_NONE;
   int rreg = 0;  // cached: the entry's cache row
+  TileSum sreg = {0, 0, 0, 0};
   auto nvalid_of = [&](int kt) { return min(PF_BK, n_vis - kt * PF_BK); };
   auto load_entries = [&](int kt) {
     const bool in = tid < PF_BK && tid < nvalid_of(kt);
     ereg = in ? ents[kt * PF_BK + tid] : PF_NONE;
     if constexpr (CACHED) rreg = in ? (int)rws[kt * PF_BK + tid] : 0;
+    if (wave == 0) sreg = tsum[kt];
   };
-  // Wave 0 writes the ring slot of tile kt; every reduction over the tile
-  // stays in scalar registers (lane reads and ballots), with no cross-lane
-  // LDS traffic on the way to the barrier that ends the step.
+  // wave 0 writes the ring slot of tile kt from the entries and the plan's
+  // summary of the tile
   auto store_entries = [&](int kt) {
     const int slot = kt % PF_ER;
     if (wave == 0) {
-      const int nvalid = nvalid_of(kt);  // >= 1: kt is a tile of the list
-      const int last = max(nvalid - 1, 0);
+      const int vr_n = __builtin_amdgcn_readfirstlane(sreg.vr_n);
+      const int nvalid = vr_n >> 8;
       ent_ring[slot][lane] = ereg;
-      // smallest rank byte of the valid entries, from the top bit down: the
-      // candidates shrink to those with a 0 in the next bit whenever any has
-      const uint32_t vr = lane < nvalid ? (ereg >> 24) : 255u;
-      uint64_t cand = ~0ull;
-      int vrmin = 0;
-#pragma unroll
-      for (int bit = 7; bit >= 0; --bit) {
-        const uint64_t z = __ballot(((vr >> bit) & 1u) == 0u) & cand;
-        if (z != 0) cand = z;
-        else vrmin |= 1 << bit;
-      }
-      const int jmin = __builtin_amdgcn_readlane((int)(ereg & 0x00ffffffu), 0);
-      const int jmax = __builtin_amdgcn_readlane((int)(ereg & 0x00ffffffu), last);
       // a padding row of the tile repeats the last valid row (its score is
       // masked, so any finite row will do)
-      if constexpr (CACHED) {
-        const int rlast = __builtin_amdgcn_readlane(rreg, last);
-        row_ring[slot][lane] = lane < nvalid ? rreg : rlast;
-      } else {
-        row_ring[slot][lane] = lane < nvalid ? (int)(ereg & 0x00ffffffu) : jmax;
-      }
+      const int row = CACHED ? rreg : (int)(ereg & 0x00ffffffu);
+      row_ring[slot][lane] = lane < nvalid ? row : __builtin_amdgcn_readfirstlane(sreg.pad_row);
       if (lane == 0) {
         TileInfo ti;
-        ti.jmin = jmin;
-        ti.jmax = jmax;
-        ti.vrmin = vrmin;
+        ti.jmin = sreg.jmin;
+        ti.jmax = sreg.jmax;
+        ti.vrmin = vr_n & 255;
         ti.nvalid = nvalid;
         info_ring[slot] = ti;
       }
@@ -600,9 +616,10 @@ __global__ __launch_bounds__(PF_THREADS) __attribute__((amdgpu_waves_per_eu(3)))
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     uint16_t* __restrict__ o, int32_t H, int32_t L, int64_t qs, int64_t kvs, int64_t os, float c2,
     const int32_t* __restrict__ vu, int32_t L_meta, const uint32_t* __restrict__ list,
-    const int32_t* __restrict__ count, int32_t n_qt, int32_t L_pad, int32_t n_work, PfCached cc) {
+    const int32_t* __restrict__ count, const TileSum* __restrict__ info, int32_t n_qt,
+    int32_t L_pad, int32_t n_work, PfCached cc) {
   prefill_attn_body<uint16_t, D, CACHED>(q, k, v, o, H, L, qs, kvs, os, c2, vu, L_meta, list,
-                                         count, n_qt, L_pad, n_work, cc);
+                                         count, info, n_qt, L_pad, n_work, cc);
 }
 
 template <int D, bool CACHED>
@@ -610,31 +627,33 @@ __global__ __launch_bounds__(PF_THREADS) void prefill_attn_kernel_f32(
     const float* __restrict__ q, const float* __restrict__ k, const float* __restrict__ v,
     float* __restrict__ o, int32_t H, int32_t L, int64_t qs, int64_t kvs, int64_t os, float c2,
     const int32_t* __restrict__ vu, int32_t L_meta, const uint32_t* __restrict__ list,
-    const int32_t* __restrict__ count, int32_t n_qt, int32_t L_pad, int32_t n_work, PfCached cc) {
+    const int32_t* __restrict__ count, const TileSum* __restrict__ info, int32_t n_qt,
+    int32_t L_pad, int32_t n_work, PfCached cc) {
   prefill_attn_body<float, D, CACHED>(q, k, v, o, H, L, qs, kvs, os, c2, vu, L_meta, list, count,
-                                      n_qt, L_pad, n_work, cc);
+                                      info, n_qt, L_pad, n_work, cc);
 }
 
 template <typename T, int D, bool CACHED>
 static int launch_prefill(const void* q, const void* k, const void* v, void* o, int32_t b,
                           int32_t H, int32_t L, int64_t qs, int64_t kvs, int64_t os, float scale,
                           const int32_t* vu, int32_t L_meta, uint32_t* list, int32_t* count,
-                          int32_t n_qt, int32_t L_pad, PfCached cc, hipStream_t stream) {
+                          TileSum* info, int32_t n_qt, int32_t L_pad, PfCached cc,
+                          hipStream_t stream) {
   prefill_plan_kernel<CACHED><<<dim3(n_qt, b), 256, 0, stream>>>(vu, L_meta, L, n_qt, L_pad, list,
-                                                                 count, cc);
+                                                                 count, info, cc);
   int rc = hip_check(hipGetLastError(), "span_masked_prefill_attn: plan launch");
   if (rc) return rc;
   const int n_work = b * H * n_qt;
   if constexpr (sizeof(T) == 2)
     prefill_attn_kernel_bf16<D, CACHED><<<n_work, PF_THREADS, 0, stream>>>(
         static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
-        static_cast<T*>(o), H, L, qs, kvs, os, scale * PF_LOG2E, vu, L_meta, list, count, n_qt,
-        L_pad, n_work, cc);
+        static_cast<T*>(o), H, L, qs, kvs, os, scale * PF_LOG2E, vu, L_meta, list, count, info,
+        n_qt, L_pad, n_work, cc);
   else
     prefill_attn_kernel_f32<D, CACHED><<<n_work, PF_THREADS, 0, stream>>>(
         static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
-        static_cast<T*>(o), H, L, qs, kvs, os, scale * PF_LOG2E, vu, L_meta, list, count, n_qt,
-        L_pad, n_work, cc);
+        static_cast<T*>(o), H, L, qs, kvs, os, scale * PF_LOG2E, vu, L_meta, list, count, info,
+        n_qt, L_pad, n_work, cc);
   return hip_check(hipGetLastError(), "span_masked_prefill_attn: launch");
 }
 
@@ -642,13 +661,13 @@ template <bool CACHED>
 static int dispatch_prefill(const void* q, const void* k, const void* v, void* o, int32_t b,
                             int32_t H, int32_t L, int32_t d_head, sckv_dtype dt, int64_t qs,
                             int64_t kvs, int64_t os, float scale, const int32_t* vu,
-                            int32_t L_meta, uint32_t* list, int32_t* cnt, int32_t n_qt,
-                            int32_t L_pad, PfCached cc, hipStream_t stream) {
+                            int32_t L_meta, uint32_t* list, int32_t* cnt, TileSum* info,
+                            int32_t n_qt, int32_t L_pad, PfCached cc, hipStream_t stream) {
   if (dt == SCKV_BF16)
-    return d_head == 64 ? launch_prefill<uint16_t, 64, CACHED>(q, k, v, o, b, H, L, qs, kvs, os, scale, vu, L_meta, list, cnt, n_qt, L_pad, cc, stream)
-                        : launch_prefill<uint16_t, 80, CACHED>(q, k, v, o, b, H, L, qs, kvs, os, scale, vu, L_meta, list, cnt, n_qt, L_pad, cc, stream);
-  return d_head == 64 ? launch_prefill<float, 64, CACHED>(q, k, v, o, b, H, L, qs, kvs, os, scale, vu, L_meta, list, cnt, n_qt, L_pad, cc, stream)
-                      : launch_prefill<float, 80, CACHED>(q, k, v, o, b, H, L, qs, kvs, os, scale, vu, L_meta, list, cnt, n_qt, L_pad, cc, stream);
+    return d_head == 64 ? launch_prefill<uint16_t, 64, CACHED>(q, k, v, o, b, H, L, qs, kvs, os, scale, vu, L_meta, list, cnt, info, n_qt, L_pad, cc, stream)
+                        : launch_prefill<uint16_t, 80, CACHED>(q, k, v, o, b, H, L, qs, kvs, os, scale, vu, L_meta, list, cnt, info, n_qt, L_pad, cc, stream);
+  return d_head == 64 ? launch_prefill<float, 64, CACHED>(q, k, v, o, b, H, L, qs, kvs, os, scale, vu, L_meta, list, cnt, info, n_qt, L_pad, cc, stream)
+                      : launch_prefill<float, 80, CACHED>(q, k, v, o, b, H, L, qs, kvs, os, scale, vu, L_meta, list, cnt, info, n_qt, L_pad, cc, stream);
 }
 
 static void plan_geometry(int32_t L, int32_t* n_qt, int32_t* L_pad) {
@@ -671,8 +690,9 @@ extern "C" size_t sckv_prefill_workspace_bytes(int32_t b, int32_t L) {
   int32_t n_qt, L_pad;
   plan_geometry(L, &n_qt, &L_pad);
   const size_t list = (size_t)b * n_qt * L_pad * sizeof(uint32_t);
+  const size_t sums = (size_t)b * n_qt * (L_pad / 64) * sizeof(TileSum);
   const size_t cnt = ((size_t)b * n_qt * sizeof(int32_t) + 255) / 256 * 256;
-  return list + cnt;
+  return list + sums + cnt;
 }
 
 extern "C" int span_masked_prefill_attn(const void* q, const void* k, const void* v, void* o,
@@ -701,10 +721,14 @@ extern "C" int span_masked_prefill_attn(const void* q, const void* k, const void
   int32_t n_qt, L_pad;
   plan_geometry(L, &n_qt, &L_pad);
   if ((int64_t)b * H * n_qt > 0x7fffffff) return fail(SCKV_EUNSUP, "span_masked_prefill_attn: grid too large");
+  // workspace: list entries | tile summaries | counts
+  const size_t list_bytes = (size_t)b * n_qt * L_pad * sizeof(uint32_t);
+  const size_t sum_bytes = (size_t)b * n_qt * (L_pad / 64) * sizeof(TileSum);
   uint32_t* list = static_cast<uint32_t*>(ws);
-  int32_t* cnt = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + (size_t)b * n_qt * L_pad * sizeof(uint32_t));
+  TileSum* sums = reinterpret_cast<TileSum*>(static_cast<char*>(ws) + list_bytes);
+  int32_t* cnt = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + list_bytes + sum_bytes);
   return dispatch_prefill<false>(q, k, v, o, b, H, L, d_head, dt, q_stride_bh, kv_stride_bh,
-                                 o_stride_bh, scale, vu, L_meta, list, cnt, n_qt, L_pad,
+                                 o_stride_bh, scale, vu, L_meta, list, cnt, sums, n_qt, L_pad,
                                  PfCached{}, stream);
 }
 
@@ -713,8 +737,9 @@ extern "C" size_t sckv_prefill_cached_workspace_bytes(int32_t b, int32_t nq, int
   int32_t n_qt, L_pad;
   plan_geometry_cached(nq, L_cap, &n_qt, &L_pad);
   const size_t list = (size_t)b * n_qt * L_pad * sizeof(uint32_t);  // entries, then rows
+  const size_t sums = (size_t)b * n_qt * (L_pad / 64) * sizeof(TileSum);
   const size_t cnt = ((size_t)b * n_qt * sizeof(int32_t) + 255) / 256 * 256;
-  return 2 * list + cnt;
+  return 2 * list + sums + cnt;
 }
 
 extern "C" int span_masked_prefill_attn_cached(
@@ -760,8 +785,11 @@ extern "C" int span_masked_prefill_attn_cached(
   cc.tok0 = tok0;
   cc.L_cap = L_cap;
   cc.status = status;
-  int32_t* cnt = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + 2 * list_bytes);
+  // workspace: list entries | their cache rows | tile summaries | counts
+  const size_t sum_bytes = (size_t)b * n_qt * (L_pad / 64) * sizeof(TileSum);
+  TileSum* sums = reinterpret_cast<TileSum*>(static_cast<char*>(ws) + 2 * list_bytes);
+  int32_t* cnt = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + 2 * list_bytes + sum_bytes);
   return dispatch_prefill<true>(q, k_cache, v_cache, o, b, H, nq, d_head, dt, q_stride_bh,
-                                kv_stride_bh, o_stride_bh, scale, vu, L_meta, list, cnt, n_qt,
-                                L_pad, cc, stream);
+                                kv_stride_bh, o_stride_bh, scale, vu, L_meta, list, cnt, sums,
+                                n_qt, L_pad, cc, stream);
 }

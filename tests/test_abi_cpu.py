@@ -158,7 +158,8 @@ def test_block_entry_points_reject_bad_arguments(B):
     assert lib.kv_extend(FAKE, FAKE, FAKE, FAKE, FAKE, 100, 0, -1, 1, 64, NULL, NULL) == B.EINVAL
     # prefill over the cache
     ws = lib.sckv_prefill_cached_workspace_bytes(2, 100, 512)
-    assert ws == 2 * (2 * 1 * 512 * 4) + 256  # entries + rows, one 128-query block; counts
+    # entries + rows (one 128-query block), 16-byte summaries of 64-entry tiles, counts
+    assert ws == 2 * (2 * 1 * 512 * 4) + 2 * 1 * (512 // 64) * 16 + 256
     assert lib.sckv_prefill_cached_workspace_bytes(0, 100, 512) == 0
 
     def call(**kw):
