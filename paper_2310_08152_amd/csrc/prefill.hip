@@ -416,8 +416,11 @@ __device__ __forceinline__ void prefill_attn_body(
     }
   };
 
+  // summary of the tile being computed, read from the ring one step early
+  // so that the step starts with its key reads
+  TileInfo tcur;
   auto compute = [&](int kt, const char* kcur, const char* vcur) {
-    const TileInfo ti = info_ring[kt % PF_ER];
+    const TileInfo ti = tcur;
     const uint32_t* tent = ent_ring[kt % PF_ER];
     if (wave_live && ti.jmin <= Iw + 31) {
       const bool full = ti.nvalid == PF_BK && ti.jmax <= Iw && ti.vrmin >= Iw + 31 - I;
@@ -536,6 +539,7 @@ __device__ __forceinline__ void prefill_attn_body(
     }
     if (kt + 2 < nt) load_entries(kt + 2);
     compute(kt, kc, vc);
+    if (kt + 1 < nt) tcur = info_ring[(kt + 1) % PF_ER];
     if constexpr (C::NBUF == 1) {
       __syncthreads();
       if (kt + 1 < nt) dma_rows(kt + 1, kn, vn);
@@ -555,6 +559,7 @@ __device__ __forceinline__ void prefill_attn_body(
   dma_rows(0, kbuf0, vbuf0);
   wait_vmem();
   __syncthreads();
+  tcur = info_ring[0];
 
   for (int kt = 0; kt < nt; kt += 2) {
     if constexpr (C::NBUF == 2) {
