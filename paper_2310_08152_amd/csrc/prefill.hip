@@ -427,16 +427,23 @@ __device__ __forceinline__ void prefill_attn_body(
       // ---- S^T = K Q^T for the two 32-key blocks ----
       f32x16 sacc[2];
 #pragma unroll
-      for (int kb2 = 0; kb2 < 2; ++kb2) {
+      for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
         for (int i = 0; i < 16; ++i) sacc[kb2][i] = 0.f;
-        if constexpr (BF) {
-          const char* krow = kcur + ((kb2 * 32 + l32) * C::KP + g * 8) * 2;
+      if constexpr (BF) {
 #pragma unroll
-          for (int kk = 0; kk < C::KSTEPS; ++kk) {
+        for (int kk = 0; kk < C::KSTEPS; ++kk) {
+#pragma unroll
+          for (int kb2 = 0; kb2 < 2; ++kb2) {
+            const char* krow = kcur + ((kb2 * 32 + l32) * C::KP + g * 8) * 2;
             const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(krow + kk * 32));
             sacc[kb2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[kk], sacc[kb2], 0, 0, 0);
           }
+        }
+      }
+#pragma unroll
+      for (int kb2 = 0; kb2 < 2; ++kb2) {
+        if constexpr (BF) {
         } else {
           const float* krow = reinterpret_cast<const float*>(kcur) + (kb2 * 32 + l32) * C::KP + g;
 #pragma unroll
@@ -505,9 +512,9 @@ __device__ __forceinline__ void prefill_attn_body(
         const int G = lane >> 4, j16 = lane & 15;
         const uint16_t* vsrc = vs + (4 * g + (j16 >> 2)) * C::VP + 16 * (G & 1) + 4 * (j16 & 3);
 #pragma unroll
-        for (int db = 0; db < NDB; ++db) {
+        for (int t = 0; t < 4; ++t) {
 #pragma unroll
-          for (int t = 0; t < 4; ++t) {
+          for (int db = 0; db < NDB; ++db) {
             const s16x4 lo = lds_read_tr16(vsrc + (16 * t) * C::VP + 32 * db);
             const s16x4 hi = lds_read_tr16(vsrc + (16 * t + 8) * C::VP + 32 * db);
             const s16x8 w = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
