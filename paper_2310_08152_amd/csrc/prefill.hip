@@ -424,31 +424,25 @@ __device__ __forceinline__ void prefill_attn_body(
     const uint32_t* tent = ent_ring[kt % PF_ER];
     if (wave_live && ti.jmin <= Iw + 31) {
       const bool full = ti.nvalid == PF_BK && ti.jmax <= Iw && ti.vrmin >= Iw + 31 - I;
-      // ---- S^T = K Q^T for the two 32-key blocks ----
+      // ---- S^T = K Q^T for the two 32-key blocks, key step outer so that
+      // consecutive matrix instructions write different accumulators ----
       f32x16 sacc[2];
 #pragma unroll
       for (int kb2 = 0; kb2 < 2; ++kb2)
 #pragma unroll
         for (int i = 0; i < 16; ++i) sacc[kb2][i] = 0.f;
-      if constexpr (BF) {
 #pragma unroll
-        for (int kk = 0; kk < C::KSTEPS; ++kk) {
+      for (int kk = 0; kk < C::KSTEPS; ++kk) {
 #pragma unroll
-          for (int kb2 = 0; kb2 < 2; ++kb2) {
-            const char* krow = kcur + ((kb2 * 32 + l32) * C::KP + g * 8) * 2;
-            const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(krow + kk * 32));
+        for (int kb2 = 0; kb2 < 2; ++kb2) {
+          if constexpr (BF) {
+            const char* krow = kcur + ((kb2 * 32 + l32) * C::KP + g * 8 + kk * 16) * 2;
+            const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(krow));
             sacc[kb2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[kk], sacc[kb2], 0, 0, 0);
-          }
-        }
-      }
-#pragma unroll
-      for (int kb2 = 0; kb2 < 2; ++kb2) {
-        if constexpr (BF) {
-        } else {
-          const float* krow = reinterpret_cast<const float*>(kcur) + (kb2 * 32 + l32) * C::KP + g;
-#pragma unroll
-          for (int kk = 0; kk < C::KSTEPS; ++kk)
+          } else {
+            const float* krow = reinterpret_cast<const float*>(kcur) + (kb2 * 32 + l32) * C::KP + g;
             sacc[kb2] = __builtin_amdgcn_mfma_f32_32x32x2f32(krow[2 * kk], qreg[kk], sacc[kb2], 0, 0, 0);
+          }
         }
       }
       // ---- element mask on tiles not entirely visible to this wave ----
