@@ -442,7 +442,9 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
   constexpr int NA = 8 * KS;     // value elements per lane
   constexpr int THREADS = NW * 64;
   constexpr int HD = D / 2;
-  static_assert(D >= 64 && D <= 128 && D % 16 == 0, "one or two elements per lane of wave 0");
+  // new-row elements: one per thread of the workgroup, then one or two per
+  // lane of wave 0 for the score
+  static_assert(D >= 64 && D <= 128 && D % 16 == 0 && D <= NW * 64, "head size");
   // chunk-major order (as in decode_chunk_kernel)
   const int n_bh = n_work / n_chunk_max;
   const int chunk = blockIdx.x / n_bh;
