@@ -332,9 +332,9 @@ def run_streaming(args, w):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py runs on exactly one GPU: the sentinel-token compression path shards "
-              "over sequences/heads/layers with no exchange, so multi-GPU figures are not "
-              "produced by this build (pass --gpus 1).", file=sys.stderr)
+        print("bench.py measures one GPU only: the sentinel-token compression path shards "
+              "over sequences/heads/layers with no exchange between GPUs, and no multi-GPU "
+              "figure is produced (pass --gpus 1).", file=sys.stderr)
         sys.exit(2)
 
     import torch
