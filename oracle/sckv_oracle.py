@@ -43,7 +43,7 @@ import numpy as np
 NORMAL, CL, CR = 0, 1, 2
 
 __all__ = [
-    "NORMAL", "CL", "CR", "token_types", "enclosing_cr", "attention_mask",
+    "NORMAL", "CL", "CR", "token_types", "enclosing_cr", "attention_mask", "attention_mask_rows",
     "tie_positions", "rope_rotate_half", "masked_attention", "keep_rows",
     "compact_cache", "decode_attention", "run_prompt_and_decode",
 ]
@@ -120,6 +120,25 @@ def attention_mask(types):
     return m
 
 
+def attention_mask_rows(types, rows):
+    """The rows ``rows`` of attention_mask(types), built pair by pair by the
+    same rules, for sequences too long for the whole L x L mask."""
+    L = len(types)
+    enc = enclosing_cr(types)
+    m = np.zeros((len(rows), L), dtype=bool)
+    for r, i in enumerate(rows):
+        for j in range(i + 1):
+            if types[i] == CL:
+                m[r, j] = (j == i)
+                continue
+            if types[j] == CL:
+                continue
+            if enc[j] >= 0 and i > enc[j]:
+                continue
+            m[r, j] = True
+    return m
+
+
 def tie_positions(types):
     """Position ids of the transformed sequence (Section 3.1, "Input
     Transformation"): sentinels take the position of the token before them,
@@ -162,7 +181,8 @@ def rope_rotate_half(x, pos, theta):
 def masked_attention(q, k, v, mask, scale=None, return_probs=False):
     """softmax(scale * q k^T restricted to ``mask``) v for one sequence.
 
-    q, k, v: [H, L, d]; mask: [L, L] bool (row attends to column).
+    q: [H, Lq, d]; k, v: [H, L, d]; mask: [Lq, L] bool (row attends to
+    column; Lq = L for the whole sequence, fewer for sampled query rows).
     """
     q = np.asarray(q, np.float64)
     k = np.asarray(k, np.float64)

@@ -161,6 +161,26 @@ def test_bruteforce_mask_equals_closed_form():
     assert n > 500
 
 
+def test_mask_rows_equal_closed_form_and_sampled_attention():
+    """attention_mask_rows (for sequences too long for the whole mask) gives
+    the closed-form rows on every span set up to L=8, in any row order, and
+    attention over sampled query rows equals those rows of the full result."""
+    for L in range(1, 9):
+        for spans in all_span_sets(L):
+            types = O.token_types(spans, L)
+            rows = list(range(L - 1, -1, -1))
+            assert np.array_equal(O.attention_mask_rows(types, rows),
+                                  closed_form_mask(spans, L)[rows]), (L, spans)
+    H, L, d = 2, 300, 8
+    spans = [(3, 40), (50, 51), (60, 200), (250, 400)]
+    types = O.token_types(spans, L)
+    q, k, v = rnd((H, L, d), 21), rnd((H, L, d), 22), rnd((H, L, d), 23)
+    full = O.masked_attention(q, k, v, O.attention_mask(types))
+    rows = [0, 3, 39, 40, 41, 60, 199, 200, 201, 250, 299]
+    part = O.masked_attention(q[:, rows], k, v, O.attention_mask_rows(types, rows))
+    np.testing.assert_allclose(part, full[:, rows], rtol=0, atol=1e-12)
+
+
 def test_bruteforce_keep_rule_and_closed_length():
     for L in range(1, 9):
         for spans in all_span_sets(L):
