@@ -445,10 +445,11 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
   // new-row elements: one per thread of the workgroup, then one or two per
   // lane of wave 0 for the score
   static_assert(D >= 64 && D <= 128 && D % 16 == 0 && D <= NW * 64, "head size");
-  // chunk-major order (as in decode_chunk_kernel)
-  const int n_bh = n_work / n_chunk_max;
-  const int chunk = blockIdx.x / n_bh;
-  const int bh = blockIdx.x % n_bh;
+  // chunk-major order (as in decode_chunk_kernel); a one-chunk launch has
+  // one workgroup per slice
+  const int n_bh = FINAL ? n_work : n_work / n_chunk_max;
+  const int chunk = FINAL ? 0 : (int)blockIdx.x / n_bh;
+  const int bh = FINAL ? (int)blockIdx.x : (int)blockIdx.x % n_bh;
   const int s = bh / H;
   const int tid = threadIdx.x;
   const int wave = tid >> 6;
@@ -477,6 +478,21 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
   const uint16_t kx_raw = k_new[(int64_t)bh * D + te];
   const uint16_t kp_raw = k_new[(int64_t)bh * D + tp];
   const uint16_t vx_raw = v_new[(int64_t)bh * D + te];
+  // A one-chunk launch (FINAL) starts its slice at row 0, so its first block
+  // is rows 32*wave.. whatever the slice length: it is issued before the
+  // length arrives (rows past the slice's end are neutralised below).
+  const uint16_t* kb = k_cache + (int64_t)bh * L_cap * D;
+  const uint16_t* vb = v_cache + (int64_t)bh * L_cap * D;
+  auto load_row = [&](int row, u32x4* kd, u32x4* vd) {
+    const uint16_t* kp = kb + (int64_t)row * D + 8 * h;
+    const uint16_t* vp = vb + (int64_t)row * D + 8 * h;
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) kd[kk] = ld16(kp + 16 * kk);
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) vd[kk] = ld16(vp + 16 * kk);
+  };
+  u32x4 kA[KS], vA[KS], kB[KS], vB[KS];
+  if constexpr (FINAL) load_row(min(32 * wave + kr, L_cap - 1), kA, vA);
   const uint32_t* qw = reinterpret_cast<const uint32_t*>(q + (int64_t)bh * D);
   uint32_t qword[HD];
 #pragma unroll
@@ -495,24 +511,27 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
   const int nblk = chunk < cp.n ? (rc - r0 + 31) / 32 : 0;
   const bool holds_new = n >= r0 && n < r1;
 
-  const uint16_t* kb = k_cache + (int64_t)bh * L_cap * D;
-  const uint16_t* vb = v_cache + (int64_t)bh * L_cap * D;
   // rows past rc re-read row rc-1 (row 0 where the chunk has no rows);
   // their scores are masked
   auto load_blk = [&](int i, u32x4* kd, u32x4* vd) {
-    const int row = max(min(r0 + 32 * i + kr, rc - 1), 0);
-    const uint16_t* kp = kb + (int64_t)row * D + 8 * h;
-    const uint16_t* vp = vb + (int64_t)row * D + 8 * h;
-#pragma unroll
-    for (int kk = 0; kk < KS; ++kk) kd[kk] = ld16(kp + 16 * kk);
-#pragma unroll
-    for (int kk = 0; kk < KS; ++kk) vd[kk] = ld16(vp + 16 * kk);
+    load_row(max(min(r0 + 32 * i + kr, rc - 1), 0), kd, vd);
   };
   // issued whether or not the wave has these blocks, so that the counter
   // waits below stay exact on every path
-  u32x4 kA[KS], vA[KS], kB[KS], vB[KS];
-  load_blk(wave, kA, vA);
-  load_blk(wave + NW, kB, vB);
+  if constexpr (FINAL) {
+    load_blk(wave + NW, kB, vB);
+    // a short slice: rows past its end were read too.  Their scores are
+    // masked; their values are zeroed so that whatever those rows hold
+    // (they may never have been written) adds exactly nothing.
+    if (32 * wave + 32 > rc) {
+      const bool a_in = 32 * wave + kr < rc;
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) vA[kk] = a_in ? vA[kk] : u32x4{0, 0, 0, 0};
+    }
+  } else {
+    load_blk(wave, kA, vA);
+    load_blk(wave + NW, kB, vB);
+  }
 
   // the step kind, with the precedence of step_kind()
   const int kind = !t_ok ? 2

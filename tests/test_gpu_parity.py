@@ -391,6 +391,36 @@ def test_decode_matches_oracle(dtype, d, theta, H):
             assert torch.equal(cache.kv[:, :, s, :, :n], before[:, :, s, :, :n])
 
 
+@pytest.mark.parametrize("dtype,H", [("bf16", 3), ("bf16", 64), ("bf16", 128), ("f32", 64)])
+def test_decode_ignores_rows_past_the_slice(dtype, H):
+    """Rows at or past kv_len may hold anything (never written, or NaN/Inf
+    bit patterns): the output over short and long slices must not change."""
+    say(f"decode past-the-slice rows dtype={dtype} H={H}")
+    L_cap, d = 600, 80
+    lens = [0, 1, 31, 37, 100, 255, 256, 599]
+    b = len(lens)
+    meta = P().SpanMeta([[] for _ in range(b)], 1000, DEV)
+    cache = P().KVCache(1, b, H, L_cap, d, W().torch_dtype(dtype), DEV)
+    cache.kv.copy_(W().randn(cache.kv.shape, seed=71, dtype=dtype).to(DEV))
+    clean = cache.kv.clone()
+    for s_, n in enumerate(lens):   # poison every row past the slice
+        cache.kv[:, 0, s_, :, n:] = float("nan")
+        cache.kv[:, 1, s_, :, n:] = float("inf")
+    cache.kv_len.copy_(torch.tensor(lens, dtype=torch.int32))
+    cache.cur_tok.copy_(torch.tensor([700 + i for i in range(b)], dtype=torch.int32))
+    ws = P().Workspace(b, H, 1, L_cap, d, DEV)
+    q, kn, vn = (rnd((b, H, d), 80 + i, dtype) for i in range(3))
+    o = torch.empty_like(q)
+    P().decode_layer(q, kn, vn, cache, 0, meta, ws, o, theta=0.0)
+    torch.cuda.synchronize()
+    assert int(cache.status) == 0
+    assert torch.isfinite(o).all()
+    Q, KN, VN, K, V, Og = f64(q), f64(kn), f64(vn), f64(clean[0, 0]), f64(clean[0, 1]), f64(o)
+    for s_, n in enumerate(lens):
+        ref = O.decode_attention(Q[s_], KN[s_], VN[s_], K[s_], V[s_], n, False)
+        assert np.abs(Og[s_] - ref).max() <= TOL[dtype], (s_, n)
+
+
 @pytest.mark.parametrize("dtype,H", [("bf16", 2), ("bf16", 256), ("bf16", 512), ("f32", 512)])
 def test_decode_reports_capacity_and_token_errors(dtype, H):
     say(f"decode status dtype={dtype} H={H}")
