@@ -262,6 +262,9 @@ int compacted_decode_attn(const void* q, const void* k_new, const void* v_new, v
  * rope_theta > 0) and value replace row t mod W (the token t - W) and
  * o[s,h] = attention of q over the W tokens t-W+1 .. t.  cur_tok is not
  * changed.  A <CL> step (vu[s][t] == t) outputs v_new and writes nothing.
+ * The ring must be full (t >= W: the W rows hold tokens t-W .. t-1 when the
+ * call is made, e.g. after a prompt of at least W tokens was loaded into
+ * it); every ring row other than the replaced one is attended as it stands.
  * Same launch shapes and workspace as compacted_decode_attn; bf16 only;
  * 0 < W < L_cap.
  * ------------------------------------------------------------------------- */
