@@ -412,13 +412,19 @@ def measure(args, w):
                 rec["t2"].record()
         else:
             cache.start_prompt(L, meta)
+            # the mask's visibility plan is the same for every layer: built once
+            if rec is not None and use_ev:
+                rec["plan"][0].record()
+            P.prefill_plan(meta, ws, b, L)
+            if rec is not None and use_ev:
+                rec["plan"][1].record()
             for m in range(M):
                 P.rope_rows(q_in[m], qr, meta, L, 0, theta)
                 P.rope_rows(k_in[m], cache.k(m), meta, L, 0, theta)
                 P.rope_rows(v_in[m], cache.v(m), meta, L, 0, 0.0)
                 if rec is not None and use_ev:
                     rec["pf"][m][0].record()
-                P.prefill_layer(qr, cache.k(m), cache.v(m), o, meta, ws, L)
+                P.prefill_layer(qr, cache.k(m), cache.v(m), o, meta, ws, L, planned=True)
                 if rec is not None and use_ev:
                     rec["pf"][m][1].record()
             if rec is not None:
@@ -448,6 +454,7 @@ def measure(args, w):
     for _ in range(args.steps):
         recs.append({"t0": E(), "t1": E(), "t2": E(), "t3": E(),
                      "pf": [(E(), E()) for _ in range(M)] if use_ev and pb == 0 else None,
+                     "plan": (E(), E()) if use_ev and pb == 0 else None,
                      "dec": [(E(), E()) for _ in range(steps)] if use_ev else None})
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
@@ -486,7 +493,10 @@ def measure(args, w):
         dec_total_ms = float(dec_step_ms.sum(axis=1).mean())
         dec_avg_ms = dec_total_ms / max(n_dec, 1)
         pf_avg_ms = float(pf_launch_ms.mean())
+        plan_ms = (float(np.mean([r["plan"][0].elapsed_time(r["plan"][1]) for r in recs]))
+                   if pb == 0 else None)
     else:
+        plan_ms = None
         dec_avg_ms = float(np.mean(decph_ms)) / max(n_dec, 1)
         pf_avg_ms = float(np.mean(pre_ms)) / M
         dec_total_ms = float(np.mean(decph_ms))
@@ -538,12 +548,15 @@ def measure(args, w):
                      "avg_launch_us": round(dec_avg_ms * 1e3, 2),
                      "bytes_per_launch": int(dec_bytes_launch),
                      "launch": dec_launch},
-        "roofline_prefill": {"bound": "mfma", "kernel": "prefill_attn_kernel (span_masked_prefill_attn)",
+        "roofline_prefill": {"bound": "mfma",
+                             "kernel": "prefill_attn_kernel (span_masked_prefill_attn_planned; "
+                                       "the plan kernel runs once per prompt, plan_us)",
                              "achieved": round(pf_tflops_alg, 1), "peak": BF16_PEAK_TFLOPS,
                              "unit": "TFLOP/s", "frac": round(pf_tflops_alg / BF16_PEAK_TFLOPS, 4),
                              "executed_tflops": round(pf_tflops_exe, 1),
                              "executed_over_algorithmic": round(pf_exe / pf_alg, 3),
                              "avg_launch_us": round(pf_avg_ms * 1e3, 1),
+                             "plan_us": None if plan_ms is None else round(plan_ms * 1e3, 1),
                              "traffic": None if pf_traffic is None else int(pf_traffic),
                              "traffic_unit": "HBM bytes per call (Q, K, V read; O written)"},
         "phases_ms": {"rope+prefill": round(float(np.mean(pre_ms)), 3),

@@ -161,6 +161,32 @@ int span_masked_prefill_attn(const void* q, const void* k, const void* v, void* 
                              size_t ws_bytes, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
+ * The same attention with the visibility plan built once per prompt.  The
+ * plan (for every query block, the key columns its rows may see) depends only
+ * on vu, b and L, the same for every layer and head (Section 3.1: the mask is
+ * a function of the token types), so a model runs sckv_prefill_plan once and
+ * span_masked_prefill_attn_planned per layer.
+ *
+ * sckv_prefill_plan: vu, L_meta, b, L and ws as for span_masked_prefill_attn;
+ *   writes the plan into ws (stream-ordered).
+ * span_masked_prefill_attn_planned: the arguments of span_masked_prefill_attn;
+ *   ws must hold a plan from sckv_prefill_plan for the same vu, b and L,
+ *   not overwritten since.  It only reads ws, so calls on one plan may run
+ *   concurrently.  With a workspace that holds no such plan the outputs are
+ *   unspecified, but nothing outside ws, q, k, v and o is accessed.
+ * span_masked_prefill_attn = sckv_prefill_plan + span_masked_prefill_attn_planned.
+ * Errors: as span_masked_prefill_attn.
+ * ------------------------------------------------------------------------- */
+int sckv_prefill_plan(const int32_t* vu, int32_t L_meta, int32_t b, int32_t L, void* ws,
+                      size_t ws_bytes, hipStream_t stream);
+int span_masked_prefill_attn_planned(const void* q, const void* k, const void* v, void* o,
+                                     int32_t b, int32_t H, int32_t L, int32_t d_head,
+                                     int64_t q_stride_bh, int64_t kv_stride_bh,
+                                     int64_t o_stride_bh, sckv_dtype dt, float scale,
+                                     const int32_t* vu, int32_t L_meta, void* ws,
+                                     size_t ws_bytes, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
  * The same masked attention for one block of the prompt whose keys and
  * values are in a (compacted) cache: block-wise processing of a prompt that
  * does not fit, freeing closed spans after each block (Section 3,

@@ -62,6 +62,10 @@ _SIGS = {
     "span_masked_prefill_attn": (ctypes.c_int, [_p, _p, _p, _p, _i32, _i32, _i32, _i32, _i64,
                                                 _i64, _i64, ctypes.c_int, _f32, _p, _i32, _p, _sz,
                                                 _p]),
+    "sckv_prefill_plan": (ctypes.c_int, [_p, _i32, _i32, _i32, _p, _sz, _p]),
+    "span_masked_prefill_attn_planned": (ctypes.c_int, [_p, _p, _p, _p, _i32, _i32, _i32, _i32,
+                                                        _i64, _i64, _i64, ctypes.c_int, _f32, _p,
+                                                        _i32, _p, _sz, _p]),
     "kv_compact": (ctypes.c_int, [_p, _p, _i32, _i32, _i32, _i32, _i32, ctypes.c_int, _p, _p, _p,
                                   _p, _p, _i32, _p, _p]),
     "sckv_decode_workspace_bytes": (_sz, [_i32, _i32, _i32, _i32]),
@@ -186,6 +190,21 @@ def span_masked_prefill_attn(q, k, v, o, b: int, H: int, L: int, d_head: int, q_
                                         q_stride_bh, kv_stride_bh, o_stride_bh, _dtype_code(q),
                                         scale, _ptr(vu), L_meta, _ptr(ws), ws.numel() *
                                         ws.element_size(), _stream(stream, q)))
+
+
+def sckv_prefill_plan(vu, L_meta: int, b: int, L: int, ws, stream=None):
+    _check(lib.sckv_prefill_plan(_ptr(vu), L_meta, b, L, _ptr(ws), ws.numel() * ws.element_size(),
+                                 _stream(stream, ws)))
+
+
+def span_masked_prefill_attn_planned(q, k, v, o, b: int, H: int, L: int, d_head: int,
+                                     q_stride_bh: int, kv_stride_bh: int, o_stride_bh: int,
+                                     scale: float, vu, L_meta: int, ws, stream=None):
+    _check(lib.span_masked_prefill_attn_planned(_ptr(q), _ptr(k), _ptr(v), _ptr(o), b, H, L,
+                                                d_head, q_stride_bh, kv_stride_bh, o_stride_bh,
+                                                _dtype_code(q), scale, _ptr(vu), L_meta, _ptr(ws),
+                                                ws.numel() * ws.element_size(),
+                                                _stream(stream, q)))
 
 
 def kv_compact(kv, kv_out, M: int, b: int, H: int, L_cap: int, d_head: int, kv_len, tok_idx,

@@ -284,7 +284,9 @@ __device__ __forceinline__ void prefill_attn_body(
       return;
     }
   }
-  const int n_vis = count[(int64_t)s * n_qt + qt];
+  // clamped into the list, so that a workspace holding no valid plan (a
+  // caller's mistake with the planned entry point) reads nothing outside it
+  const int n_vis = min(max(count[(int64_t)s * n_qt + qt], 0), L_pad);
   const int nt = (n_vis + PF_BK - 1) / PF_BK;
 
   // Padding value rows/columns are written once and never again.  For bf16
@@ -647,12 +649,14 @@ template <typename T, int D, bool CACHED>
 static int launch_prefill(const void* q, const void* k, const void* v, void* o, int32_t b,
                           int32_t H, int32_t L, int64_t qs, int64_t kvs, int64_t os, float scale,
                           const int32_t* vu, int32_t L_meta, uint32_t* list, int32_t* count,
-                          TileSum* info, int32_t n_qt, int32_t L_pad, PfCached cc,
+                          TileSum* info, int32_t n_qt, int32_t L_pad, PfCached cc, bool plan,
                           hipStream_t stream) {
-  prefill_plan_kernel<CACHED><<<dim3(n_qt, b), 256, 0, stream>>>(vu, L_meta, L, n_qt, L_pad, list,
-                                                                 count, info, cc);
-  int rc = hip_check(hipGetLastError(), "span_masked_prefill_attn: plan launch");
-  if (rc) return rc;
+  if (plan) {
+    prefill_plan_kernel<CACHED><<<dim3(n_qt, b), 256, 0, stream>>>(vu, L_meta, L, n_qt, L_pad,
+                                                                   list, count, info, cc);
+    int rc = hip_check(hipGetLastError(), "span_masked_prefill_attn: plan launch");
+    if (rc) return rc;
+  }
   const int n_work = b * H * n_qt;
   if constexpr (sizeof(T) == 2)
     prefill_attn_kernel_bf16<D, CACHED><<<n_work, PF_THREADS, 0, stream>>>(
@@ -672,12 +676,13 @@ static int dispatch_prefill(const void* q, const void* k, const void* v, void* o
                             int32_t H, int32_t L, int32_t d_head, sckv_dtype dt, int64_t qs,
                             int64_t kvs, int64_t os, float scale, const int32_t* vu,
                             int32_t L_meta, uint32_t* list, int32_t* cnt, TileSum* info,
-                            int32_t n_qt, int32_t L_pad, PfCached cc, hipStream_t stream) {
+                            int32_t n_qt, int32_t L_pad, PfCached cc, bool plan,
+                            hipStream_t stream) {
   if (dt == SCKV_BF16)
-    return d_head == 64 ? launch_prefill<uint16_t, 64, CACHED>(q, k, v, o, b, H, L, qs, kvs, os, scale, vu, L_meta, list, cnt, info, n_qt, L_pad, cc, stream)
-                        : launch_prefill<uint16_t, 80, CACHED>(q, k, v, o, b, H, L, qs, kvs, os, scale, vu, L_meta, list, cnt, info, n_qt, L_pad, cc, stream);
-  return d_head == 64 ? launch_prefill<float, 64, CACHED>(q, k, v, o, b, H, L, qs, kvs, os, scale, vu, L_meta, list, cnt, info, n_qt, L_pad, cc, stream)
-                      : launch_prefill<float, 80, CACHED>(q, k, v, o, b, H, L, qs, kvs, os, scale, vu, L_meta, list, cnt, info, n_qt, L_pad, cc, stream);
+    return d_head == 64 ? launch_prefill<uint16_t, 64, CACHED>(q, k, v, o, b, H, L, qs, kvs, os, scale, vu, L_meta, list, cnt, info, n_qt, L_pad, cc, plan, stream)
+                        : launch_prefill<uint16_t, 80, CACHED>(q, k, v, o, b, H, L, qs, kvs, os, scale, vu, L_meta, list, cnt, info, n_qt, L_pad, cc, plan, stream);
+  return d_head == 64 ? launch_prefill<float, 64, CACHED>(q, k, v, o, b, H, L, qs, kvs, os, scale, vu, L_meta, list, cnt, info, n_qt, L_pad, cc, plan, stream)
+                      : launch_prefill<float, 80, CACHED>(q, k, v, o, b, H, L, qs, kvs, os, scale, vu, L_meta, list, cnt, info, n_qt, L_pad, cc, plan, stream);
 }
 
 static void plan_geometry(int32_t L, int32_t* n_qt, int32_t* L_pad) {
@@ -705,41 +710,97 @@ extern "C" size_t sckv_prefill_workspace_bytes(int32_t b, int32_t L) {
   return list + sums + cnt;
 }
 
+// workspace of the plain prefill: list entries | tile summaries | counts
+struct PlainPlan {
+  uint32_t* list;
+  TileSum* sums;
+  int32_t* cnt;
+  int32_t n_qt, L_pad;
+};
+static PlainPlan plain_plan(void* ws, int32_t b, int32_t L) {
+  PlainPlan p;
+  plan_geometry(L, &p.n_qt, &p.L_pad);
+  const size_t list_bytes = (size_t)b * p.n_qt * p.L_pad * sizeof(uint32_t);
+  const size_t sum_bytes = (size_t)b * p.n_qt * (p.L_pad / 64) * sizeof(TileSum);
+  p.list = static_cast<uint32_t*>(ws);
+  p.sums = reinterpret_cast<TileSum*>(static_cast<char*>(ws) + list_bytes);
+  p.cnt = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + list_bytes + sum_bytes);
+  return p;
+}
+
+// checks shared by the plan-only call and the attention calls
+static int check_plan_args(const char* W, const int32_t* vu, int32_t b, int32_t L, int32_t L_meta,
+                           const void* ws, size_t ws_bytes) {
+  if (!vu || !ws) return fail(SCKV_EINVAL, std::string(W) + ": null pointer");
+  if (b <= 0 || L <= 0) return fail(SCKV_EINVAL, std::string(W) + ": sizes must be positive");
+  if (L > 32768) return fail(SCKV_EUNSUP, std::string(W) + ": L above 32768");
+  if (L_meta < L) return fail(SCKV_EINVAL, std::string(W) + ": L_meta < L");
+  if (!aligned16(ws)) return fail(SCKV_EINVAL, std::string(W) + ": workspace must be 16-byte aligned");
+  if (ws_bytes < sckv_prefill_workspace_bytes(b, L))
+    return fail(SCKV_EINVAL, std::string(W) + ": workspace too small");
+  return SCKV_OK;
+}
+
+static int prefill_entry(const char* W, bool plan, const void* q, const void* k, const void* v,
+                         void* o, int32_t b, int32_t H, int32_t L, int32_t d_head,
+                         int64_t q_stride_bh, int64_t kv_stride_bh, int64_t o_stride_bh,
+                         sckv_dtype dt, float scale, const int32_t* vu, int32_t L_meta, void* ws,
+                         size_t ws_bytes, hipStream_t stream) {
+  clear_error();
+  if (!q || !k || !v || !o) return fail(SCKV_EINVAL, std::string(W) + ": null pointer");
+  int rc = check_plan_args(W, vu, b, L, L_meta, ws, ws_bytes);
+  if (rc) return rc;
+  if (!valid_dtype(dt)) return fail(SCKV_EINVAL, std::string(W) + ": unknown dtype");
+  if (!supported_d(d_head)) return fail(SCKV_EUNSUP, std::string(W) + ": d_head must be 64 or 80");
+  if (H <= 0) return fail(SCKV_EINVAL, std::string(W) + ": sizes must be positive");
+  const int64_t rowlen = (int64_t)L * d_head;
+  if (q_stride_bh < rowlen || kv_stride_bh < rowlen || o_stride_bh < rowlen)
+    return fail(SCKV_EINVAL, std::string(W) + ": slice stride smaller than L*d_head");
+  const int eb = elem_bytes(dt);
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) ||
+      (q_stride_bh * eb) % 16 || (kv_stride_bh * eb) % 16 || (o_stride_bh * eb) % 16)
+    return fail(SCKV_EINVAL, std::string(W) + ": buffers and strides must be 16-byte aligned");
+  if (!(scale > 0.f) || std::isinf(scale)) return fail(SCKV_EINVAL, std::string(W) + ": scale must be finite and > 0");
+  const PlainPlan p = plain_plan(ws, b, L);
+  if ((int64_t)b * H * p.n_qt > 0x7fffffff) return fail(SCKV_EUNSUP, std::string(W) + ": grid too large");
+  return dispatch_prefill<false>(q, k, v, o, b, H, L, d_head, dt, q_stride_bh, kv_stride_bh,
+                                 o_stride_bh, scale, vu, L_meta, p.list, p.cnt, p.sums, p.n_qt,
+                                 p.L_pad, PfCached{}, plan, stream);
+}
+
 extern "C" int span_masked_prefill_attn(const void* q, const void* k, const void* v, void* o,
                                         int32_t b, int32_t H, int32_t L, int32_t d_head,
                                         int64_t q_stride_bh, int64_t kv_stride_bh,
                                         int64_t o_stride_bh, sckv_dtype dt, float scale,
                                         const int32_t* vu, int32_t L_meta, void* ws,
                                         size_t ws_bytes, hipStream_t stream) {
+  return prefill_entry("span_masked_prefill_attn", true, q, k, v, o, b, H, L, d_head, q_stride_bh,
+                       kv_stride_bh, o_stride_bh, dt, scale, vu, L_meta, ws, ws_bytes, stream);
+}
+
+extern "C" int sckv_prefill_plan(const int32_t* vu, int32_t L_meta, int32_t b, int32_t L,
+                                 void* ws, size_t ws_bytes, hipStream_t stream) {
   clear_error();
-  if (!q || !k || !v || !o || !vu || !ws) return fail(SCKV_EINVAL, "span_masked_prefill_attn: null pointer");
-  if (!valid_dtype(dt)) return fail(SCKV_EINVAL, "span_masked_prefill_attn: unknown dtype");
-  if (!supported_d(d_head)) return fail(SCKV_EUNSUP, "span_masked_prefill_attn: d_head must be 64 or 80");
-  if (b <= 0 || H <= 0 || L <= 0) return fail(SCKV_EINVAL, "span_masked_prefill_attn: sizes must be positive");
-  if (L > 32768) return fail(SCKV_EUNSUP, "span_masked_prefill_attn: L above 32768");
-  if (L_meta < L) return fail(SCKV_EINVAL, "span_masked_prefill_attn: L_meta < L");
-  const int64_t rowlen = (int64_t)L * d_head;
-  if (q_stride_bh < rowlen || kv_stride_bh < rowlen || o_stride_bh < rowlen)
-    return fail(SCKV_EINVAL, "span_masked_prefill_attn: slice stride smaller than L*d_head");
-  const int eb = elem_bytes(dt);
-  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(ws) ||
-      (q_stride_bh * eb) % 16 || (kv_stride_bh * eb) % 16 || (o_stride_bh * eb) % 16)
-    return fail(SCKV_EINVAL, "span_masked_prefill_attn: buffers and strides must be 16-byte aligned");
-  if (!(scale > 0.f) || std::isinf(scale)) return fail(SCKV_EINVAL, "span_masked_prefill_attn: scale must be finite and > 0");
-  if (ws_bytes < sckv_prefill_workspace_bytes(b, L))
-    return fail(SCKV_EINVAL, "span_masked_prefill_attn: workspace too small");
-  int32_t n_qt, L_pad;
-  plan_geometry(L, &n_qt, &L_pad);
-  if ((int64_t)b * H * n_qt > 0x7fffffff) return fail(SCKV_EUNSUP, "span_masked_prefill_attn: grid too large");
-  // workspace: list entries | tile summaries | counts
-  const size_t list_bytes = (size_t)b * n_qt * L_pad * sizeof(uint32_t);
-  const size_t sum_bytes = (size_t)b * n_qt * (L_pad / 64) * sizeof(TileSum);
-  uint32_t* list = static_cast<uint32_t*>(ws);
-  TileSum* sums = reinterpret_cast<TileSum*>(static_cast<char*>(ws) + list_bytes);
-  int32_t* cnt = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + list_bytes + sum_bytes);
-  return dispatch_prefill<false>(q, k, v, o, b, H, L, d_head, dt, q_stride_bh, kv_stride_bh,
-                                 o_stride_bh, scale, vu, L_meta, list, cnt, sums, n_qt, L_pad,
-                                 PfCached{}, stream);
+  const char* W = "sckv_prefill_plan";
+  int rc = check_plan_args(W, vu, b, L, L_meta, ws, ws_bytes);
+  if (rc) return rc;
+  const PlainPlan p = plain_plan(ws, b, L);
+  prefill_plan_kernel<false><<<dim3(p.n_qt, b), 256, 0, stream>>>(vu, L_meta, L, p.n_qt, p.L_pad,
+                                                                  p.list, p.cnt, p.sums,
+                                                                  PfCached{});
+  return hip_check(hipGetLastError(), "sckv_prefill_plan: launch");
+}
+
+extern "C" int span_masked_prefill_attn_planned(const void* q, const void* k, const void* v,
+                                                void* o, int32_t b, int32_t H, int32_t L,
+                                                int32_t d_head, int64_t q_stride_bh,
+                                                int64_t kv_stride_bh, int64_t o_stride_bh,
+                                                sckv_dtype dt, float scale, const int32_t* vu,
+                                                int32_t L_meta, void* ws, size_t ws_bytes,
+                                                hipStream_t stream) {
+  return prefill_entry("span_masked_prefill_attn_planned", false, q, k, v, o, b, H, L, d_head,
+                       q_stride_bh, kv_stride_bh, o_stride_bh, dt, scale, vu, L_meta, ws,
+                       ws_bytes, stream);
 }
 
 extern "C" size_t sckv_prefill_cached_workspace_bytes(int32_t b, int32_t nq, int32_t L_cap) {
@@ -801,5 +862,5 @@ extern "C" int span_masked_prefill_attn_cached(
   int32_t* cnt = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + 2 * list_bytes + sum_bytes);
   return dispatch_prefill<true>(q, k_cache, v_cache, o, b, H, nq, d_head, dt, q_stride_bh,
                                 kv_stride_bh, o_stride_bh, scale, vu, L_meta, list, cnt, sums,
-                                n_qt, L_pad, cc, stream);
+                                n_qt, L_pad, cc, true, stream);
 }

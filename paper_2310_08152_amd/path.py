@@ -5,7 +5,8 @@ done here; every step runs in libsckv.so kernels.
 Typical use (one batch of sequences):
     meta  = SpanMeta(spans, L_meta, device)          # span metadata, tied positions
     cache = KVCache(M, b, H, L_cap, d, dtype, device)
-    for m in layers: prefill_layer(...)               # rotary + masked attention
+    prefill_plan(...)                                 # the mask's visibility plan, once
+    for m in layers: prefill_layer(..., planned=True) # rotary + masked attention
     cache.compact(meta, next_tok)                     # free closed spans in place
     for step: for m: decode_layer(...); commit(...)   # generate
 
@@ -108,12 +109,21 @@ def rope_rows(x, y, meta: SpanMeta, n: int, tok0: int, theta: float, stream=None
                  stream=stream)
 
 
-def prefill_layer(q, k, v, o, meta: SpanMeta, ws: Workspace, L: int, scale=None, stream=None):
-    """Masked attention of q (b,H,L,d) over key/value slices k, v (b,H,>=L,d)."""
+def prefill_layer(q, k, v, o, meta: SpanMeta, ws: Workspace, L: int, scale=None, stream=None,
+                  planned: bool = False):
+    """Masked attention of q (b,H,L,d) over key/value slices k, v (b,H,>=L,d).
+    With planned=True the visibility plan already in ws (prefill_plan) is
+    used instead of being rebuilt: it is the same for every layer."""
     b, H, _, d = q.shape
-    B.span_masked_prefill_attn(q, k, v, o, b, H, L, d, q.stride(1), k.stride(1), o.stride(1),
-                               default_scale(d) if scale is None else scale, meta.vu,
-                               meta.L_meta, ws.prefill, stream=stream)
+    f = B.span_masked_prefill_attn_planned if planned else B.span_masked_prefill_attn
+    f(q, k, v, o, b, H, L, d, q.stride(1), k.stride(1), o.stride(1),
+      default_scale(d) if scale is None else scale, meta.vu, meta.L_meta, ws.prefill,
+      stream=stream)
+
+
+def prefill_plan(meta: SpanMeta, ws: Workspace, b: int, L: int, stream=None):
+    """Visibility plan of the prompt's first L tokens, shared by all layers."""
+    B.sckv_prefill_plan(meta.vu, meta.L_meta, b, L, ws.prefill, stream=stream)
 
 
 def decode_layer(q, k_new, v_new, cache: KVCache, m: int, meta: SpanMeta, ws: Workspace, o,

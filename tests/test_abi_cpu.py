@@ -84,6 +84,30 @@ def test_prefill_rejects(B):
              B.F32, 0.1, FAKE, 256, FAKE, ws, NULL) == B.EINVAL
 
 
+def test_prefill_plan_rejects(B):
+    ws = B.lib.sckv_prefill_workspace_bytes(2, 300)
+    plan = B.lib.sckv_prefill_plan
+    assert plan(NULL, 300, 2, 300, FAKE, ws, NULL) == B.EINVAL
+    assert plan(FAKE, 300, 2, 300, NULL, ws, NULL) == B.EINVAL
+    assert plan(FAKE, 300, 0, 300, FAKE, ws, NULL) == B.EINVAL
+    assert plan(FAKE, 299, 2, 300, FAKE, ws, NULL) == B.EINVAL      # L_meta < L
+    assert plan(FAKE, 300, 2, 300, FAKE, ws - 1, NULL) == B.EINVAL  # workspace too small
+    assert plan(FAKE, 40000, 2, 40000, FAKE, ws, NULL) == B.EUNSUP  # L above 32768
+    assert plan(FAKE, 300, 2, 300, ctypes.c_void_p(4104), ws, NULL) == B.EINVAL  # misaligned
+    f = B.lib.span_masked_prefill_attn_planned
+    def call(**kw):
+        a = dict(b=2, H=4, L=300, d=80, s=300 * 80, dt=B.BF16, scale=0.1, ws=ws)
+        a.update(kw)
+        return f(FAKE, FAKE, FAKE, FAKE, a["b"], a["H"], a["L"], a["d"], a["s"], a["s"], a["s"],
+                 a["dt"], a["scale"], FAKE, 300, FAKE, a["ws"], NULL)
+    assert call(d=72) == B.EUNSUP
+    assert call(H=0) == B.EINVAL
+    assert call(s=100) == B.EINVAL
+    assert call(ws=ws - 1) == B.EINVAL
+    assert call(scale=float("inf")) == B.EINVAL
+    assert "planned" in B.last_error()
+
+
 def test_compact_rejects(B):
     f = B.lib.kv_compact
     args = [FAKE, NULL, 2, 1, 4, 128, 64, B.BF16, FAKE, FAKE, FAKE, FAKE, FAKE, 128, FAKE, NULL]

@@ -208,6 +208,34 @@ def test_prefill_matches_oracle(name, dtype, b, H, L, d, kind):
     assert worst <= TOL[dtype], worst
 
 
+@pytest.mark.parametrize("dtype,d", [("bf16", 80), ("f32", 64)])
+def test_prefill_plan_reuse_bitexact(dtype, d):
+    """One plan (sckv_prefill_plan) serves several layers: each planned call
+    equals span_masked_prefill_attn, which rebuilds the plan, bit for bit."""
+    say(f"prefill plan reuse dtype={dtype} d={d}")
+    b, H, L = 2, 3, 777
+    rng = np.random.default_rng(77)
+    spans = make_spans("uniform", b, L, rng)
+    meta = P().SpanMeta(spans, L, DEV)
+    ws = P().Workspace(b, H, L, L, d, DEV)
+    layers = [tuple(rnd((b, H, L, d), 400 + 10 * m + i, dtype) for i in range(3)) for m in range(3)]
+    P().prefill_plan(meta, ws, b, L)
+    planned = []
+    for q, k, v in layers:
+        o = torch.full_like(q, float("nan"))
+        P().prefill_layer(q, k, v, o, meta, ws, L, planned=True)
+        planned.append(o)
+    torch.cuda.synchronize()
+    for (q, k, v), o in zip(layers, planned):
+        ref = run_prefill(q, k, v, spans)  # plans again, in its own workspace
+        assert torch.equal(o, ref)
+    # the last layer against the oracle as well
+    q, k, v = layers[-1]
+    worst = max(np.abs(f64(planned[-1])[s_, h] - r).max()
+                for (s_, h), r in oracle_prefill(q, k, v, spans).items())
+    assert worst <= TOL[dtype], worst
+
+
 def test_prefill_eviction_invariance_bitexact():
     say("prefill eviction invariance")
     b, H, L, d = 2, 4, 1100, 64
