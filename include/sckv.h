@@ -217,6 +217,31 @@ int span_masked_prefill_attn_cached(const void* q, const void* k_cache, const vo
                                     void* ws, size_t ws_bytes, int32_t* status,
                                     hipStream_t stream);
 
+/* The cached attention with its plan built once per block: the plan (for
+ * every query block, the cache rows its rows may see) depends on vu, tok0,
+ * row0, tok_idx, L_cap, b and nq, not on the layer, so block-wise processing
+ * runs sckv_prefill_cached_plan once per block and the planned call per layer.
+ * sckv_prefill_cached_plan: arguments as for span_masked_prefill_attn_cached;
+ *   writes the plan into ws (stream-ordered).
+ * span_masked_prefill_attn_cached_planned: the arguments of
+ *   span_masked_prefill_attn_cached; ws must hold a plan from
+ *   sckv_prefill_cached_plan for the same vu, tok0, row0, tok_idx contents,
+ *   L_cap, b and nq, not overwritten since.  With a workspace that holds no
+ *   such plan the outputs are unspecified, but nothing outside ws and the
+ *   argument buffers is accessed.
+ * Errors: as span_masked_prefill_attn_cached. */
+int sckv_prefill_cached_plan(const int32_t* vu, int32_t L_meta, int32_t tok0, const int32_t* row0,
+                             const int32_t* tok_idx, int32_t L_cap, int32_t b, int32_t nq,
+                             void* ws, size_t ws_bytes, hipStream_t stream);
+int span_masked_prefill_attn_cached_planned(const void* q, const void* k_cache,
+                                            const void* v_cache, void* o, int32_t b, int32_t H,
+                                            int32_t nq, int32_t d_head, int64_t q_stride_bh,
+                                            int64_t kv_stride_bh, int64_t o_stride_bh,
+                                            sckv_dtype dt, float scale, const int32_t* vu,
+                                            int32_t L_meta, int32_t tok0, const int32_t* row0,
+                                            const int32_t* tok_idx, int32_t L_cap, void* ws,
+                                            size_t ws_bytes, int32_t* status, hipStream_t stream);
+
 /* ---------------------------------------------------------------------------
  * Free the key/value rows of closed spans, in place, keeping the survivors in
  * their order (stable stream compaction).

@@ -58,6 +58,12 @@ _SIGS = {
                                                        _i64, _i64, _i64, ctypes.c_int, _f32, _p,
                                                        _i32, _i32, _p, _p, _i32, _p, _sz, _p,
                                                        _p]),
+    "sckv_prefill_cached_plan": (ctypes.c_int, [_p, _i32, _i32, _p, _p, _i32, _i32, _i32, _p,
+                                                _sz, _p]),
+    "span_masked_prefill_attn_cached_planned": (ctypes.c_int, [_p, _p, _p, _p, _i32, _i32, _i32,
+                                                               _i32, _i64, _i64, _i64,
+                                                               ctypes.c_int, _f32, _p, _i32, _i32,
+                                                               _p, _p, _i32, _p, _sz, _p, _p]),
     "kv_extend": (ctypes.c_int, [_p, _p, _p, _p, _p, _i32, _i32, _i32, _i32, _i32, _p, _p]),
     "span_masked_prefill_attn": (ctypes.c_int, [_p, _p, _p, _p, _i32, _i32, _i32, _i32, _i64,
                                                 _i64, _i64, ctypes.c_int, _f32, _p, _i32, _p, _sz,
@@ -167,6 +173,25 @@ def span_masked_prefill_attn_cached(q, k_cache, v_cache, o, b: int, H: int, nq: 
                                     scale: float, vu, L_meta: int, tok0: int, row0, tok_idx,
                                     L_cap: int, ws, status=None, stream=None):
     _check(lib.span_masked_prefill_attn_cached(
+        _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(o), b, H, nq, d_head, q_stride_bh,
+        kv_stride_bh, o_stride_bh, _dtype_code(q), scale, _ptr(vu), L_meta, tok0, _ptr(row0),
+        _ptr(tok_idx), L_cap, _ptr(ws), ws.numel() * ws.element_size(), _ptr(status),
+        _stream(stream, q)))
+
+
+def sckv_prefill_cached_plan(vu, L_meta: int, tok0: int, row0, tok_idx, L_cap: int, b: int,
+                             nq: int, ws, stream=None):
+    _check(lib.sckv_prefill_cached_plan(_ptr(vu), L_meta, tok0, _ptr(row0), _ptr(tok_idx), L_cap,
+                                        b, nq, _ptr(ws), ws.numel() * ws.element_size(),
+                                        _stream(stream, ws)))
+
+
+def span_masked_prefill_attn_cached_planned(q, k_cache, v_cache, o, b: int, H: int, nq: int,
+                                            d_head: int, q_stride_bh: int, kv_stride_bh: int,
+                                            o_stride_bh: int, scale: float, vu, L_meta: int,
+                                            tok0: int, row0, tok_idx, L_cap: int, ws, status=None,
+                                            stream=None):
+    _check(lib.span_masked_prefill_attn_cached_planned(
         _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(o), b, H, nq, d_head, q_stride_bh,
         kv_stride_bh, o_stride_bh, _dtype_code(q), scale, _ptr(vu), L_meta, tok0, _ptr(row0),
         _ptr(tok_idx), L_cap, _ptr(ws), ws.numel() * ws.element_size(), _ptr(status),

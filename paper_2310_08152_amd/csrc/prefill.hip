@@ -813,19 +813,40 @@ extern "C" size_t sckv_prefill_cached_workspace_bytes(int32_t b, int32_t nq, int
   return 2 * list + sums + cnt;
 }
 
-extern "C" int span_masked_prefill_attn_cached(
-    const void* q, const void* k_cache, const void* v_cache, void* o, int32_t b, int32_t H,
-    int32_t nq, int32_t d_head, int64_t q_stride_bh, int64_t kv_stride_bh, int64_t o_stride_bh,
-    sckv_dtype dt, float scale, const int32_t* vu, int32_t L_meta, int32_t tok0,
-    const int32_t* row0, const int32_t* tok_idx, int32_t L_cap, void* ws, size_t ws_bytes,
-    int32_t* status, hipStream_t stream) {
-  clear_error();
-  const char* W = "span_masked_prefill_attn_cached";
-  if (!q || !k_cache || !v_cache || !o || !vu || !row0 || !tok_idx || !ws)
-    return fail(SCKV_EINVAL, std::string(W) + ": null pointer");
-  if (!valid_dtype(dt)) return fail(SCKV_EINVAL, std::string(W) + ": unknown dtype");
-  if (!supported_d(d_head)) return fail(SCKV_EUNSUP, std::string(W) + ": d_head must be 64 or 80");
-  if (b <= 0 || H <= 0 || nq <= 0 || L_cap <= 0)
+// workspace of the cached prefill: list entries | their cache rows | tile
+// summaries | counts
+struct CachedPlan {
+  uint32_t* list;
+  TileSum* sums;
+  int32_t* cnt;
+  PfCached cc;
+  int32_t n_qt, L_pad;
+};
+static CachedPlan cached_plan(void* ws, int32_t b, int32_t nq, int32_t L_cap, int32_t tok0,
+                              const int32_t* row0, const int32_t* tok_idx, int32_t* status) {
+  CachedPlan p;
+  plan_geometry_cached(nq, L_cap, &p.n_qt, &p.L_pad);
+  const size_t list_bytes = (size_t)b * p.n_qt * p.L_pad * sizeof(uint32_t);
+  const size_t sum_bytes = (size_t)b * p.n_qt * (p.L_pad / 64) * sizeof(TileSum);
+  char* base = static_cast<char*>(ws);
+  p.list = reinterpret_cast<uint32_t*>(base);
+  p.cc.rows = reinterpret_cast<uint32_t*>(base + list_bytes);
+  p.sums = reinterpret_cast<TileSum*>(base + 2 * list_bytes);
+  p.cnt = reinterpret_cast<int32_t*>(base + 2 * list_bytes + sum_bytes);
+  p.cc.row0 = row0;
+  p.cc.tok = tok_idx;
+  p.cc.tok0 = tok0;
+  p.cc.L_cap = L_cap;
+  p.cc.status = status;
+  return p;
+}
+
+// checks shared by the cached plan-only call and the cached attention calls
+static int check_cached_plan_args(const char* W, const int32_t* vu, int32_t L_meta, int32_t tok0,
+                                  const int32_t* row0, const int32_t* tok_idx, int32_t L_cap,
+                                  int32_t b, int32_t nq, const void* ws, size_t ws_bytes) {
+  if (!vu || !row0 || !tok_idx || !ws) return fail(SCKV_EINVAL, std::string(W) + ": null pointer");
+  if (b <= 0 || nq <= 0 || L_cap <= 0)
     return fail(SCKV_EINVAL, std::string(W) + ": sizes must be positive");
   if (L_cap > 32768 || nq > L_cap) return fail(SCKV_EUNSUP, std::string(W) + ": nq <= L_cap <= 32768 required");
   // list entries hold a token in 24 bits; 0xffffff marks padding
@@ -833,34 +854,73 @@ extern "C" int span_masked_prefill_attn_cached(
     return fail(SCKV_EUNSUP, std::string(W) + ": L_meta must be in (0, 2^24 - 1)");
   if (tok0 < 0 || (int64_t)tok0 + nq > L_meta)
     return fail(SCKV_EINVAL, std::string(W) + ": query tokens [tok0, tok0+nq) exceed L_meta");
+  if (!aligned16(ws)) return fail(SCKV_EINVAL, std::string(W) + ": workspace must be 16-byte aligned");
+  if (ws_bytes < sckv_prefill_cached_workspace_bytes(b, nq, L_cap))
+    return fail(SCKV_EINVAL, std::string(W) + ": workspace too small");
+  return SCKV_OK;
+}
+
+static int cached_entry(const char* W, bool plan, const void* q, const void* k_cache,
+                        const void* v_cache, void* o, int32_t b, int32_t H, int32_t nq,
+                        int32_t d_head, int64_t q_stride_bh, int64_t kv_stride_bh,
+                        int64_t o_stride_bh, sckv_dtype dt, float scale, const int32_t* vu,
+                        int32_t L_meta, int32_t tok0, const int32_t* row0, const int32_t* tok_idx,
+                        int32_t L_cap, void* ws, size_t ws_bytes, int32_t* status,
+                        hipStream_t stream) {
+  clear_error();
+  if (!q || !k_cache || !v_cache || !o) return fail(SCKV_EINVAL, std::string(W) + ": null pointer");
+  int rc = check_cached_plan_args(W, vu, L_meta, tok0, row0, tok_idx, L_cap, b, nq, ws, ws_bytes);
+  if (rc) return rc;
+  if (!valid_dtype(dt)) return fail(SCKV_EINVAL, std::string(W) + ": unknown dtype");
+  if (!supported_d(d_head)) return fail(SCKV_EUNSUP, std::string(W) + ": d_head must be 64 or 80");
+  if (H <= 0) return fail(SCKV_EINVAL, std::string(W) + ": sizes must be positive");
   if (q_stride_bh < (int64_t)nq * d_head || o_stride_bh < (int64_t)nq * d_head ||
       kv_stride_bh < (int64_t)L_cap * d_head)
     return fail(SCKV_EINVAL, std::string(W) + ": slice stride too small");
   const int eb = elem_bytes(dt);
   if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(o) ||
-      !aligned16(ws) || (q_stride_bh * eb) % 16 || (kv_stride_bh * eb) % 16 ||
-      (o_stride_bh * eb) % 16)
+      (q_stride_bh * eb) % 16 || (kv_stride_bh * eb) % 16 || (o_stride_bh * eb) % 16)
     return fail(SCKV_EINVAL, std::string(W) + ": buffers and strides must be 16-byte aligned");
   if (!(scale > 0.f) || std::isinf(scale)) return fail(SCKV_EINVAL, std::string(W) + ": scale must be finite and > 0");
-  if (ws_bytes < sckv_prefill_cached_workspace_bytes(b, nq, L_cap))
-    return fail(SCKV_EINVAL, std::string(W) + ": workspace too small");
-  int32_t n_qt, L_pad;
-  plan_geometry_cached(nq, L_cap, &n_qt, &L_pad);
-  if ((int64_t)b * H * n_qt > 0x7fffffff) return fail(SCKV_EUNSUP, std::string(W) + ": grid too large");
-  const size_t list_bytes = (size_t)b * n_qt * L_pad * sizeof(uint32_t);
-  uint32_t* list = static_cast<uint32_t*>(ws);
-  PfCached cc;
-  cc.rows = reinterpret_cast<uint32_t*>(static_cast<char*>(ws) + list_bytes);
-  cc.row0 = row0;
-  cc.tok = tok_idx;
-  cc.tok0 = tok0;
-  cc.L_cap = L_cap;
-  cc.status = status;
-  // workspace: list entries | their cache rows | tile summaries | counts
-  const size_t sum_bytes = (size_t)b * n_qt * (L_pad / 64) * sizeof(TileSum);
-  TileSum* sums = reinterpret_cast<TileSum*>(static_cast<char*>(ws) + 2 * list_bytes);
-  int32_t* cnt = reinterpret_cast<int32_t*>(static_cast<char*>(ws) + 2 * list_bytes + sum_bytes);
+  const CachedPlan p = cached_plan(ws, b, nq, L_cap, tok0, row0, tok_idx, status);
+  if ((int64_t)b * H * p.n_qt > 0x7fffffff) return fail(SCKV_EUNSUP, std::string(W) + ": grid too large");
   return dispatch_prefill<true>(q, k_cache, v_cache, o, b, H, nq, d_head, dt, q_stride_bh,
-                                kv_stride_bh, o_stride_bh, scale, vu, L_meta, list, cnt, sums,
-                                n_qt, L_pad, cc, true, stream);
+                                kv_stride_bh, o_stride_bh, scale, vu, L_meta, p.list, p.cnt,
+                                p.sums, p.n_qt, p.L_pad, p.cc, plan, stream);
+}
+
+extern "C" int span_masked_prefill_attn_cached(
+    const void* q, const void* k_cache, const void* v_cache, void* o, int32_t b, int32_t H,
+    int32_t nq, int32_t d_head, int64_t q_stride_bh, int64_t kv_stride_bh, int64_t o_stride_bh,
+    sckv_dtype dt, float scale, const int32_t* vu, int32_t L_meta, int32_t tok0,
+    const int32_t* row0, const int32_t* tok_idx, int32_t L_cap, void* ws, size_t ws_bytes,
+    int32_t* status, hipStream_t stream) {
+  return cached_entry("span_masked_prefill_attn_cached", true, q, k_cache, v_cache, o, b, H, nq,
+                      d_head, q_stride_bh, kv_stride_bh, o_stride_bh, dt, scale, vu, L_meta, tok0,
+                      row0, tok_idx, L_cap, ws, ws_bytes, status, stream);
+}
+
+extern "C" int sckv_prefill_cached_plan(const int32_t* vu, int32_t L_meta, int32_t tok0,
+                                        const int32_t* row0, const int32_t* tok_idx,
+                                        int32_t L_cap, int32_t b, int32_t nq, void* ws,
+                                        size_t ws_bytes, hipStream_t stream) {
+  clear_error();
+  const char* W = "sckv_prefill_cached_plan";
+  int rc = check_cached_plan_args(W, vu, L_meta, tok0, row0, tok_idx, L_cap, b, nq, ws, ws_bytes);
+  if (rc) return rc;
+  const CachedPlan p = cached_plan(ws, b, nq, L_cap, tok0, row0, tok_idx, nullptr);
+  prefill_plan_kernel<true><<<dim3(p.n_qt, b), 256, 0, stream>>>(vu, L_meta, nq, p.n_qt, p.L_pad,
+                                                                 p.list, p.cnt, p.sums, p.cc);
+  return hip_check(hipGetLastError(), "sckv_prefill_cached_plan: launch");
+}
+
+extern "C" int span_masked_prefill_attn_cached_planned(
+    const void* q, const void* k_cache, const void* v_cache, void* o, int32_t b, int32_t H,
+    int32_t nq, int32_t d_head, int64_t q_stride_bh, int64_t kv_stride_bh, int64_t o_stride_bh,
+    sckv_dtype dt, float scale, const int32_t* vu, int32_t L_meta, int32_t tok0,
+    const int32_t* row0, const int32_t* tok_idx, int32_t L_cap, void* ws, size_t ws_bytes,
+    int32_t* status, hipStream_t stream) {
+  return cached_entry("span_masked_prefill_attn_cached_planned", false, q, k_cache, v_cache, o, b,
+                      H, nq, d_head, q_stride_bh, kv_stride_bh, o_stride_bh, dt, scale, vu,
+                      L_meta, tok0, row0, tok_idx, L_cap, ws, ws_bytes, status, stream);
 }

@@ -136,15 +136,22 @@ def decode_layer(q, k_new, v_new, cache: KVCache, m: int, meta: SpanMeta, ws: Wo
 
 
 def prefill_block(q, cache: KVCache, m: int, o, meta: SpanMeta, ws: Workspace, tok0: int, row0,
-                  scale=None, stream=None):
+                  scale=None, stream=None, planned: bool = False):
     """Masked attention of a block's queries q (b,H,nq,d), tokens tok0.., over
-    layer m of the cache, whose rows row0.. hold the block itself."""
+    layer m of the cache, whose rows row0.. hold the block itself.  With
+    planned=True the plan already in ws (prefill_block_plan) is used."""
     b, H, nq, d = q.shape
-    B.span_masked_prefill_attn_cached(q, cache.k(m), cache.v(m), o, b, H, nq, d, q.stride(1),
-                                      cache.k(m).stride(1), o.stride(1),
-                                      default_scale(d) if scale is None else scale, meta.vu,
-                                      meta.L_meta, tok0, row0, cache.tok_idx, cache.L_cap,
-                                      ws.prefill_cached, status=cache.status, stream=stream)
+    f = B.span_masked_prefill_attn_cached_planned if planned else B.span_masked_prefill_attn_cached
+    f(q, cache.k(m), cache.v(m), o, b, H, nq, d, q.stride(1), cache.k(m).stride(1), o.stride(1),
+      default_scale(d) if scale is None else scale, meta.vu, meta.L_meta, tok0, row0,
+      cache.tok_idx, cache.L_cap, ws.prefill_cached, status=cache.status, stream=stream)
+
+
+def prefill_block_plan(cache: KVCache, meta: SpanMeta, ws: Workspace, tok0: int, nq: int, row0,
+                       stream=None):
+    """Plan of a block's masked attention over the cache, shared by all layers."""
+    B.sckv_prefill_cached_plan(meta.vu, meta.L_meta, tok0, row0, cache.tok_idx, cache.L_cap,
+                               cache.b, nq, ws.prefill_cached, stream=stream)
 
 
 def prefill_progressive(q, k, v, o, cache: KVCache, meta: SpanMeta, ws: Workspace, L: int,
@@ -167,6 +174,7 @@ def prefill_progressive(q, k, v, o, cache: KVCache, meta: SpanMeta, ws: Workspac
     for B0 in range(0, L, block):
         n = min(block, L - B0)
         cache.extend(meta, B0, n, row0, stream=stream)
+        prefill_block_plan(cache, meta, ws, B0, n, row0, stream=stream)
         for m in range(M):
             for kv, src, th in ((0, k, theta), (1, v, 0.0)):
                 x = src[m, :, :, B0:B0 + n]
@@ -177,7 +185,7 @@ def prefill_progressive(q, k, v, o, cache: KVCache, meta: SpanMeta, ws: Workspac
             B.rope_apply(q[m, :, :, B0:B0 + n], qr, b, H, n, q.stride(2), qr.stride(1), d,
                          meta.pos, meta.L_meta, B0, theta, stream=stream)
             prefill_block(qr[:, :, :n], cache, m, o[m, :, :, B0:B0 + n], meta, ws, B0, row0,
-                          scale=scale, stream=stream)
+                          scale=scale, stream=stream, planned=True)
         nxt.fill_(B0 + n)
         cache.compact(meta, next_tok=nxt, stream=stream)
         if on_block is not None:

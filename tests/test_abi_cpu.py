@@ -203,6 +203,32 @@ def test_block_entry_points_reject_bad_arguments(B):
     assert call(ws=ws - 1) == B.EINVAL
     assert call(d=96) == B.EUNSUP
     assert call(scale=0.0) == B.EINVAL
+    # the same checks on the planned call, and the plan's own
+    def planned(**kw):
+        a = dict(b=2, H=2, nq=100, d=64, qs=100 * 64, kvs=512 * 64, os=100 * 64, dt=B.BF16,
+                 scale=0.125, L_meta=1000, tok0=0, row0=FAKE, tok=FAKE, L_cap=512, ws=ws)
+        a.update(kw)
+        return lib.span_masked_prefill_attn_cached_planned(
+            FAKE, FAKE, FAKE, FAKE, a["b"], a["H"], a["nq"], a["d"], a["qs"], a["kvs"], a["os"],
+            a["dt"], a["scale"], FAKE, a["L_meta"], a["tok0"], a["row0"], a["tok"], a["L_cap"],
+            FAKE, a["ws"], NULL, NULL)
+    assert planned(kvs=256 * 64) == B.EINVAL
+    assert planned(d=96) == B.EUNSUP
+    assert planned(tok0=950) == B.EINVAL
+    assert "planned" in B.last_error()
+
+    def plan(**kw):
+        a = dict(L_meta=1000, tok0=0, row0=FAKE, tok=FAKE, L_cap=512, b=2, nq=100, ws=ws)
+        a.update(kw)
+        return lib.sckv_prefill_cached_plan(FAKE, a["L_meta"], a["tok0"], a["row0"], a["tok"],
+                                            a["L_cap"], a["b"], a["nq"], FAKE, a["ws"], NULL)
+    assert plan(row0=NULL) == B.EINVAL
+    assert plan(nq=600) == B.EUNSUP
+    assert plan(L_meta=1 << 24) == B.EUNSUP
+    assert plan(tok0=950) == B.EINVAL
+    assert plan(ws=ws - 1) == B.EINVAL
+    assert plan(b=0) == B.EINVAL
+    assert "cached_plan" in B.last_error()
 
 
 def test_local_decode_rejects_bad_arguments(B):

@@ -159,3 +159,48 @@ def test_progressive_block_without_room_reports_capacity():
     assert int(cache.kv_len[0]) == 118  # first block only, compacted
     assert torch.isfinite(o[0, 0, 0, :128].float()).all()
     assert torch.isnan(o[0, 0, 0, 128:].float()).all()
+
+
+@pytest.mark.parametrize("dtype,d", [("bf16", 80), ("f32", 64)])
+def test_block_plan_reuse_bitexact(dtype, d):
+    """Block by block, with freeing between blocks: a plan built once per
+    block (sckv_prefill_cached_plan) serves every layer, and each planned
+    call equals span_masked_prefill_attn_cached, which plans again, bit for
+    bit."""
+    say(f"block plan reuse dtype={dtype} d={d}")
+    M, b, H, L, block, theta = 2, 2, 2, 400, 128, 1e4
+    rng = np.random.default_rng(4242)
+    spans = spans_for("random", b, L, rng)
+    x = [W().randn((M, b, H, L, d), seed=870 + i, dtype=dtype, device=DEV) for i in range(3)]
+    q, k, v = x
+    meta = P().SpanMeta(spans, L, DEV)
+    cache = P().KVCache(M, b, H, L, d, W().torch_dtype(dtype), DEV)
+    ws = P().Workspace(b, H, block, L, d, DEV, block=block)
+    ws2 = P().Workspace(b, H, block, L, d, DEV, block=block)  # for the calls that plan again
+    B = P().B
+    cache.kv_len.zero_()
+    row0 = torch.empty(b, dtype=torch.int32, device=DEV)
+    nxt = torch.empty(b, dtype=torch.int32, device=DEV)
+    qr = torch.empty(b, H, block, d, dtype=q.dtype, device=DEV)
+    for B0 in range(0, L, block):
+        n = min(block, L - B0)
+        cache.extend(meta, B0, n, row0)
+        P().prefill_block_plan(cache, meta, ws, B0, n, row0)
+        for m in range(M):
+            for kv, src, th in ((0, k, theta), (1, v, 0.0)):
+                xs = src[m, :, :, B0:B0 + n]
+                dst = cache.kv[m, kv]
+                B.rope_apply_at(xs, dst, row0, cache.L_cap, b, H, n, xs.stride(1), dst.stride(1),
+                                d, meta.pos, meta.L_meta, B0, th, status=cache.status)
+            B.rope_apply(q[m, :, :, B0:B0 + n], qr, b, H, n, q.stride(2), qr.stride(1), d,
+                         meta.pos, meta.L_meta, B0, theta)
+            o1 = torch.full((b, H, n, d), float("nan"), dtype=q.dtype, device=DEV)
+            o2 = torch.full_like(o1, float("nan"))
+            P().prefill_block(qr[:, :, :n], cache, m, o1, meta, ws, B0, row0, planned=True)
+            P().prefill_block(qr[:, :, :n], cache, m, o2, meta, ws2, B0, row0)
+            torch.cuda.synchronize()
+            assert torch.equal(o1, o2), (B0, m)
+            assert torch.isfinite(o1).all()
+        nxt.fill_(B0 + n)
+        cache.compact(meta, next_tok=nxt)
+    assert int(cache.status) == 0
