@@ -83,7 +83,7 @@ __device__ int first_moving_rank(const int32_t* __restrict__ ks, int n, int* sh)
   const int wave = tid >> 6;
   if (n <= 0) return 0;
   const int S = (n + MOVE_THREADS - 1) / MOVE_THREADS;  // segment length
-  // round 1: probe the last rank of every segment
+  // first pass: probe the last rank of every segment
   int seg_end = tid * S + S - 1;
   if (seg_end > n - 1) seg_end = n - 1;
   const bool moved = (tid * S < n) && (ks[seg_end] != seg_end);
@@ -94,7 +94,7 @@ __device__ int first_moving_rank(const int32_t* __restrict__ ks, int n, int* sh)
   for (int w = 0; w < MOVE_THREADS / 64; ++w) t0 = min(t0, sh[w]);
   __syncthreads();
   if (t0 == 0x7fffffff) return n;
-  // round 2: probe every rank of segment t0 (S <= MOVE_THREADS when n <= 65536)
+  // second pass: probe every rank of segment t0 (S <= MOVE_THREADS when n <= 65536)
   const int r = t0 * S + tid;
   const bool moved2 = (tid < S) && (r < n) && (ks[r] != r);
   const uint64_t m2 = __ballot(moved2);
