@@ -98,7 +98,9 @@ def run_decode_workload(w, steps, samples, check, prefill_layer=None, prefill_he
         P().rope_rows(qi, qr, meta, L, 0, theta)
         P().rope_rows(ki, cache.k(m), meta, L, 0, theta)
         o = torch.empty_like(qi)
-        P().prefill_layer(qr, cache.k(m), cache.v(m), o, meta, ws, L)
+        # the sequence bench.py times: the prompt's plan once, then the planned layer call
+        P().prefill_plan(meta, ws, b, L)
+        P().prefill_layer(qr, cache.k(m), cache.v(m), o, meta, ws, L, planned=True)
         torch.cuda.synchronize()
         for s, h in prefill_heads:
             say(f"  prefill oracle s={s} h={h}")
