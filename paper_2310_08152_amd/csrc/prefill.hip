@@ -323,6 +323,10 @@ __device__ __forceinline__ void prefill_attn_body(
     }
   }
 
+  // a <CL> row's output is its own value row; the flag is read here, where
+  // the load overlaps the staging of the first tiles, not after the loop
+  const bool is_cl = qrow < L && vu[(int64_t)s * L_meta + qtok] == qtok;
+
   f32x16 oacc[NDB];
 #pragma unroll
   for (int db = 0; db < NDB; ++db)
@@ -333,19 +337,27 @@ __device__ __forceinline__ void prefill_attn_body(
   // ---- staging: list entries run two tiles ahead through an LDS ring; the
   // key/value rows of tile kt+1 go global -> LDS by direct loads addressed
   // from the ring while tile kt is multiplied ----
-  uint32_t ereg = PF_NONE;
-  int rreg = 0;  // cached: the entry's cache row
-  TileSum sreg = {0, 0, 0, 0};
+  // a tile's list entries (wave 0's lanes), their cache rows (cached) and the
+  // plan's summary of the tile, between their load and their ring slot
+  struct Staged {
+    uint32_t e;
+    int r;
+    TileSum s;
+  };
+  Staged stg = {PF_NONE, 0, {0, 0, 0, 0}};
   auto nvalid_of = [&](int kt) { return min(PF_BK, n_vis - kt * PF_BK); };
-  auto load_entries = [&](int kt) {
+  auto load_entries = [&](int kt, Staged& st) {
     const bool in = tid < PF_BK && tid < nvalid_of(kt);
-    ereg = in ? ents[kt * PF_BK + tid] : PF_NONE;
-    if constexpr (CACHED) rreg = in ? (int)rws[kt * PF_BK + tid] : 0;
-    if (wave == 0) sreg = tsum[kt];
+    st.e = in ? ents[kt * PF_BK + tid] : PF_NONE;
+    if constexpr (CACHED) st.r = in ? (int)rws[kt * PF_BK + tid] : 0;
+    if (wave == 0) st.s = tsum[kt];
   };
   // wave 0 writes the ring slot of tile kt from the entries and the plan's
   // summary of the tile
-  auto store_entries = [&](int kt) {
+  auto store_entries = [&](int kt, const Staged& st) {
+    const uint32_t ereg = st.e;
+    const int rreg = st.r;
+    const TileSum sreg = st.s;
     const int slot = kt % PF_ER;
     if (wave == 0) {
       const int vr_n = __builtin_amdgcn_readfirstlane(sreg.vr_n);
@@ -544,7 +556,7 @@ __device__ __forceinline__ void prefill_attn_body(
     if constexpr (C::NBUF == 2) {
       if (kt + 1 < nt) dma_rows(kt + 1, kn, vn);
     }
-    if (kt + 2 < nt) load_entries(kt + 2);
+    if (kt + 2 < nt) load_entries(kt + 2, stg);
     compute(kt, kc, vc);
     if (kt + 1 < nt) tcur = info_ring[(kt + 1) % PF_ER];
     if constexpr (C::NBUF == 1) {
@@ -552,15 +564,17 @@ __device__ __forceinline__ void prefill_attn_body(
       if (kt + 1 < nt) dma_rows(kt + 1, kn, vn);
     }
     wait_vmem();
-    if (kt + 2 < nt) store_entries(kt + 2);
+    if (kt + 2 < nt) store_entries(kt + 2, stg);
     __syncthreads();
   };
 
-  load_entries(0);
-  store_entries(0);
-  if (nt > 1) {
-    load_entries(1);
-    store_entries(1);
+  // tiles 0 and 1 staged with one round trip: both loads before either store
+  {
+    Staged st1 = {PF_NONE, 0, {0, 0, 0, 0}};
+    load_entries(0, stg);
+    if (nt > 1) load_entries(1, st1);
+    store_entries(0, stg);
+    if (nt > 1) store_entries(1, st1);
   }
   __syncthreads();
   dma_rows(0, kbuf0, vbuf0);
@@ -590,7 +604,6 @@ __device__ __forceinline__ void prefill_attn_body(
   }
   if (qrow >= L) return;
   const float inv = 1.f / l_tot;
-  const bool is_cl = vu[(int64_t)s * L_meta + qtok] == qtok;
   T* orow = o + (int64_t)bh * os + (int64_t)qrow * D;
   const T* vrow = vb + (int64_t)(own_row0 + qrow) * D;
 #pragma unroll
