@@ -46,6 +46,8 @@ namespace sckv {
 constexpr int PF_WAVES = 4;
 constexpr int PF_BQ = 32 * PF_WAVES;
 constexpr int PF_BK = 64;
+// a block's list has room for at least two tiles (its first two are loaded early)
+static_assert(PF_BQ >= 2 * PF_BK, "list of at least two tiles");
 constexpr int PF_THREADS = 64 * PF_WAVES;
 constexpr uint32_t PF_NONE = 0x00ffffffu;  // list entry of a padding column
 constexpr float PF_LOG2E = 1.4426950408889634f;
@@ -323,9 +325,23 @@ __device__ __forceinline__ void prefill_attn_body(
     }
   }
 
-  // a <CL> row's output is its own value row; the flag is read here, where
-  // the load overlaps the staging of the first tiles, not after the loop
+  // A <CL> row's output is its own value row.  It is copied here, where its
+  // loads overlap the staging of the first tiles, rather than after the loop
+  // (the epilogue then writes only the other rows).
   const bool is_cl = qrow < L && vu[(int64_t)s * L_meta + qtok] == qtok;
+  T* const orow = o + (int64_t)bh * os + (int64_t)qrow * D;
+  if (is_cl) {
+    const T* vrow = vb + (int64_t)(own_row0 + qrow) * D;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const int d0 = db * 32 + 8 * jj + 4 * g;
+        if (d0 >= D) continue;
+        if constexpr (BF) *reinterpret_cast<u32x2*>(orow + d0) = *reinterpret_cast<const u32x2*>(vrow + d0);
+        else st16(orow + d0, ld16(vrow + d0));
+      }
+  }
 
   f32x16 oacc[NDB];
 #pragma unroll
@@ -346,17 +362,22 @@ __device__ __forceinline__ void prefill_attn_body(
   };
   Staged stg = {PF_NONE, 0, {0, 0, 0, 0}};
   auto nvalid_of = [&](int kt) { return min(PF_BK, n_vis - kt * PF_BK); };
+  // The loads do not depend on the list's length (tile kt < max(nt, 2) lies
+  // inside the block's list of L_pad >= 128 entries), so the first tiles'
+  // loads need not wait for the count; the length masks them when stored.
   auto load_entries = [&](int kt, Staged& st) {
-    const bool in = tid < PF_BK && tid < nvalid_of(kt);
-    st.e = in ? ents[kt * PF_BK + tid] : PF_NONE;
-    if constexpr (CACHED) st.r = in ? (int)rws[kt * PF_BK + tid] : 0;
+    if (tid < PF_BK) {
+      st.e = ents[kt * PF_BK + tid];
+      if constexpr (CACHED) st.r = (int)rws[kt * PF_BK + tid];
+    }
     if (wave == 0) st.s = tsum[kt];
   };
   // wave 0 writes the ring slot of tile kt from the entries and the plan's
   // summary of the tile
   auto store_entries = [&](int kt, const Staged& st) {
-    const uint32_t ereg = st.e;
-    const int rreg = st.r;
+    const bool in = lane < nvalid_of(kt);
+    const uint32_t ereg = in ? st.e : PF_NONE;
+    const int rreg = in ? st.r : 0;
     const TileSum sreg = st.s;
     const int slot = kt % PF_ER;
     if (wave == 0) {
@@ -568,11 +589,12 @@ __device__ __forceinline__ void prefill_attn_body(
     __syncthreads();
   };
 
-  // tiles 0 and 1 staged with one round trip: both loads before either store
+  // tiles 0 and 1 staged with one round trip: both loads (issued without
+  // waiting for the list's length) before either store
   {
     Staged st1 = {PF_NONE, 0, {0, 0, 0, 0}};
     load_entries(0, stg);
-    if (nt > 1) load_entries(1, st1);
+    load_entries(1, st1);
     store_entries(0, stg);
     if (nt > 1) store_entries(1, st1);
   }
@@ -592,7 +614,7 @@ __device__ __forceinline__ void prefill_attn_body(
     }
   }
 
-  // ---- epilogue: normalise and write; a <CL> row copies its value row ----
+  // ---- epilogue: normalise and write (<CL> rows were written at the start) ----
   if (!wave_live) return;
   float l_tot;
   if constexpr (ONES_SUM) {
@@ -602,10 +624,8 @@ __device__ __forceinline__ void prefill_attn_body(
   } else {
     l_tot = l_run + __shfl_xor(l_run, 32, 64);
   }
-  if (qrow >= L) return;
+  if (qrow >= L || is_cl) return;
   const float inv = 1.f / l_tot;
-  T* orow = o + (int64_t)bh * os + (int64_t)qrow * D;
-  const T* vrow = vb + (int64_t)(own_row0 + qrow) * D;
 #pragma unroll
   for (int db = 0; db < NDB; ++db)
 #pragma unroll
@@ -614,21 +634,13 @@ __device__ __forceinline__ void prefill_attn_body(
       if (d0 >= D) continue;
       if constexpr (BF) {
         u32x2 w;
-        if (is_cl) {
-          w = *reinterpret_cast<const u32x2*>(vrow + d0);
-        } else {
-          w[0] = pack_bf16x2(oacc[db][4 * jj] * inv, oacc[db][4 * jj + 1] * inv);
-          w[1] = pack_bf16x2(oacc[db][4 * jj + 2] * inv, oacc[db][4 * jj + 3] * inv);
-        }
+        w[0] = pack_bf16x2(oacc[db][4 * jj] * inv, oacc[db][4 * jj + 1] * inv);
+        w[1] = pack_bf16x2(oacc[db][4 * jj + 2] * inv, oacc[db][4 * jj + 3] * inv);
         *reinterpret_cast<u32x2*>(orow + d0) = w;
       } else {
         u32x4 w;
-        if (is_cl) {
-          w = ld16(vrow + d0);
-        } else {
 #pragma unroll
-          for (int i = 0; i < 4; ++i) w[i] = __float_as_uint(oacc[db][4 * jj + i] * inv);
-        }
+        for (int i = 0; i < 4; ++i) w[i] = __float_as_uint(oacc[db][4 * jj + i] * inv);
         st16(orow + d0, w);
       }
     }
