@@ -2,6 +2,8 @@
 
   stats   KERNEL_STATS_CSV TITLE COMMAND        -> markdown table (stdout)
   traffic FETCH_CSV WRITE_CSV OUT_JSON ...     -> calibrated HBM bytes per dispatch
+  pmc     OUT_MD TITLE --csv ... --kernel ...  -> MFMA busy share, executed MFMA flops,
+                                                 instruction mix per dispatch
 
 `traffic` reads two `rocprofv3 --pmc FETCH_SIZE` / `--pmc WRITE_SIZE` runs of
 the same program (counter_collection.csv, values in KiB per dispatch),
