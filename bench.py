@@ -137,6 +137,24 @@ def stored_traffic(name, workload):
     return sum(k["hbm_bytes"] for k in d["kernels"].values())
 
 
+def stored_mfma_busy(name, workload, kernel):
+    """Share of the matrix cores' clocks a kernel kept busy, from a stored SQ
+    counter summary, or None if it is missing, for another workload, or taken
+    from kernel sources that have changed since."""
+    path = os.path.join(ROOT, "profiles", name)
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        d = json.load(f)
+    from paper_2310_08152_amd.rocprof_summary import sources_hash
+    if d.get("workload") != workload:
+        return None
+    if sources_hash([os.path.join(ROOT, x) for x in d["sources"]]) != d["sources_hash"]:
+        return None
+    k = d["kernels"].get(kernel, {})
+    return None if "mfma_busy" not in k else round(k["mfma_busy"], 4)
+
+
 # ---------------------------------------------------------------------------
 # CPU baseline: the oracle on a bounded sample
 # ---------------------------------------------------------------------------
@@ -558,7 +576,11 @@ def measure(args, w):
                              "avg_launch_us": round(pf_avg_ms * 1e3, 1),
                              "plan_us": None if plan_ms is None else round(plan_ms * 1e3, 1),
                              "traffic": None if pf_traffic is None else int(pf_traffic),
-                             "traffic_unit": "HBM bytes per call (Q, K, V read; O written)"},
+                             "traffic_unit": "HBM bytes per call (Q, K, V read; O written)",
+                             "mfma_busy": stored_mfma_busy("mfma_3b-rope.json", wl_key,
+                                                           "prefill_attn_kernel"),
+                             "mfma_busy_unit": "share of the matrix cores' clocks busy "
+                                               "(SQ counters, profiles/mfma_3b-rope_bench.md)"},
         "phases_ms": {"rope+prefill": round(float(np.mean(pre_ms)), 3),
                       "compaction": round(float(np.mean(cmp_ms)), 3),
                       "decode": round(float(np.mean(decph_ms)), 3)},

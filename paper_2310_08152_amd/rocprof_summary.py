@@ -176,6 +176,14 @@ def cmd_pmc(args):
             f"{n} {v:,.0f}" for n, v in sorted(r["counters"].items())))
     for note in args.note or []:
         lines += ["", note]
+    if args.json:
+        d = {"workload": args.workload, "commands": args.command, "sources": args.sources,
+             "sources_hash": sources_hash([os.path.join(os.path.dirname(PKG), x)
+                                           for x in args.sources]),
+             "kernels": {k: {n: v for n, v in r.items() if n != "counters"}
+                         for k, r in out.items()}}
+        with open(args.json, "w") as f:
+            json.dump(d, f, indent=1)
     with open(args.out, "w") as f:
         f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
@@ -212,6 +220,9 @@ def main(argv=None):
     m.add_argument("--bf16-peak", type=float, default=2500.0, help="TFLOP/s")
     m.add_argument("--peak-clock", type=float, default=2.4, help="GHz the peak is quoted at")
     m.add_argument("--note", action="append", help="paragraph appended to the summary")
+    m.add_argument("--json", help="also write the derived figures here, with a hash of --sources")
+    m.add_argument("--workload", default=None)
+    m.add_argument("--sources", nargs="+", default=[])
     a = ap.parse_args(argv)
     {"stats": cmd_stats, "traffic": cmd_traffic, "pmc": cmd_pmc}[a.cmd](a)
 

@@ -51,8 +51,13 @@ def test_pmc_mfma_share_and_flops(tmp_path):
                   (8, 1, "other", "SQ_WAVES", 5.0, t0, t1)])
     write_csv(b, [(7, 1, "k_attn<80>", "SQ_INSTS_VALU", 500.0, t0, t1 + 1000),
                   (7, 1, "k_attn<80>", "SQ_WAIT_ANY", 400.0, t0, t1 + 1000)])
+    js = tmp_path / "o.json"
     R.main(["pmc", str(out), "t", "--csv", str(a), "--csv", str(b), "--command", "c",
-            "--kernel", "k_attn"])
+            "--kernel", "k_attn", "--json", str(js), "--workload", "w",
+            "--sources", "paper_2310_08152_amd/rocprof_summary.py"])
+    d = json.load(open(js))
+    assert d["workload"] == "w" and len(d["sources_hash"]) == 16
+    assert d["kernels"]["k_attn"]["mfma_busy"] == 0.25
     text = open(out).read()
     row = [ln for ln in text.splitlines() if ln.startswith("| `k_attn`")][0].split("|")
     clock, share, tflops = float(row[4]), float(row[5]), float(row[6])
