@@ -580,7 +580,7 @@ def measure(args, w):
                              "mfma_busy": stored_mfma_busy("mfma_3b-rope.json", wl_key,
                                                            "prefill_attn_kernel"),
                              "mfma_busy_unit": "share of the matrix cores' clocks busy "
-                                               "(SQ counters, profiles/mfma_3b-rope_bench.md)"},
+                                               "(SQ counters, profiles/mfma_3b-rope.json)"},
         "phases_ms": {"rope+prefill": round(float(np.mean(pre_ms)), 3),
                       "compaction": round(float(np.mean(cmp_ms)), 3),
                       "decode": round(float(np.mean(decph_ms)), 3)},
