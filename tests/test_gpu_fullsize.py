@@ -70,10 +70,28 @@ def oracle_slice(K0, V0, L, types, pos, qd, kd, vd, theta, cr_steps, check):
     return out
 
 
-def run_decode_workload(w, steps, samples, check, prefill_layer=None, prefill_heads=()):
+def row_schedule(types, L, steps, cr_steps):
+    """Rows the cache holds when each generated token attends (the token's
+    own row included), from the oracle's keep rule; index i is step i+1."""
+    n = int(O.keep_rows(types, L)[:L].sum())
+    out = []
+    for t in range(L, L + steps):
+        out.append(n + 1)
+        if types[t] != O.CL:
+            n += 1
+        if t in cr_steps:
+            n = int(O.keep_rows(types, t + 1)[:t + 1].sum())
+    return out
+
+
+def run_decode_workload(w, steps, samples, check, prefill_layer=None, prefill_heads=(),
+                        L_cap=None):
     """Fill the cache with the prompt (rotary keys for the prefill layer),
     optionally run prefill on one layer, compact at the end of the prompt,
-    run `steps` decode steps over all layers, and check samples."""
+    run `steps` decode steps over all layers, and check samples.  Every
+    sequence's length, token indices and positions are compared with the
+    oracle's bookkeeping after the prompt's compaction and after the last
+    step."""
     M, b, H, d, L = w.layers, w.batch, w.heads, w.d_head, w.seq_len
     theta = w.rope_theta
     T = L + steps
@@ -81,7 +99,8 @@ def run_decode_workload(w, steps, samples, check, prefill_layer=None, prefill_he
     types = [O.token_types(s, T) for s in spans]
     pos = [O.tie_positions(t) for t in types]
     keep_n = [int(O.keep_rows(t, L)[:L].sum()) for t in types]
-    L_cap = max(L, max(keep_n) + steps)
+    if L_cap is None:
+        L_cap = max(L, max(keep_n) + steps)
     meta = P().SpanMeta(spans, T, DEV)
     cache = P().KVCache(M, b, H, L_cap, d, torch.bfloat16, DEV)
     ws = P().Workspace(b, H, L, L_cap, d, DEV)
@@ -147,6 +166,25 @@ def run_decode_workload(w, steps, samples, check, prefill_layer=None, prefill_he
             cache.compact(meta)
     torch.cuda.synchronize()
     assert int(cache.status) == 0
+    cr_set = set(cr_steps)
+    for s in range(b):
+        ref = O.compact_cache(np.zeros((1, L, 1)), np.zeros((1, L, 1)), np.arange(L),
+                              pos[s][:L].copy(), L, types[s], L)
+        tok = np.zeros(T, np.int64); pp = np.zeros(T, np.int64)
+        n = ref[4]
+        tok[:n], pp[:n] = ref[2][:n], ref[3][:n]
+        for t in range(L, T):
+            if types[s][t] != O.CL:
+                tok[n], pp[n] = t, pos[s][t]
+                n += 1
+            if t in cr_set:
+                keep = O.keep_rows(types[s], t + 1)
+                kept = [r for r in range(n) if keep[tok[r]]]
+                tok[:len(kept)], pp[:len(kept)] = tok[kept], pp[kept]
+                n = len(kept)
+        assert int(cache.kv_len[s]) == n, (s, int(cache.kv_len[s]), n)
+        assert np.array_equal(cache.tok_idx[s, :n].cpu().numpy(), tok[:n])
+        assert np.array_equal(cache.pos_ids[s, :n].cpu().numpy(), pp[:n])
     Q, K, V = f64(qd), f64(kd), f64(vd)
     for (m, s, h), (K0, V0) in before.items():
         say(f"  decode oracle m={m} s={s} h={h}")
@@ -182,12 +220,29 @@ def test_fullsize_opt13b_compact_decode():
     run_decode_workload(w, w.decode_steps, samples, check={1, 64, 128})
 
 
-def test_fullsize_streaming_batch256_short():
-    """The streaming workload at full batch (b=256, 32 layers, d=80, prompt
-    1024) for its first 120 generated tokens (two spans close)."""
+def test_fullsize_streaming_batch256():
+    """The streaming workload over its whole schedule: b=256, 32 layers,
+    H=32, d=80, rotary, a 1024-token prompt and 1024 generated tokens in
+    which a span of 32 closes every 48 tokens (21 closes, one span still
+    open at the end), compacted in place after every <CR>.  The cache is
+    sized to the schedule's peak row count, as the benchmark sizes it.
+    Sampled (layer, sequence, head) outputs are checked at the first step,
+    right after the 1st, 11th and 21st compactions, at the step that attends
+    to the most rows, and at the last step."""
     w = W().get_workload("3b-rope-stream")
-    say(f"full size {w.name} (120 generated tokens)")
+    steps = w.gen_tokens
+    L, T = w.seq_len, w.seq_len + steps
+    spans = [(c, r) for c, r in W().workload_spans(w)[0] if c < T]
+    types = O.token_types(spans, T)
+    cr_steps = sorted(r for _, r in spans if L <= r < T)
+    assert len(cr_steps) == 21
+    rows = row_schedule(types, L, steps, set(cr_steps))
+    peak_step = int(np.argmax(rows)) + 1
+    after = [cr_steps[k] - L + 2 for k in (0, 10, 20)]  # the step right after each close
+    check = {1, peak_step, steps, *after}
+    say(f"full size {w.name} ({steps} generated tokens): peak {max(rows)} rows at step "
+        f"{peak_step}; checks at steps {sorted(check)}")
     rng = np.random.default_rng(5)
     samples = [(int(rng.integers(w.layers)), int(rng.integers(w.batch)), int(rng.integers(w.heads)))
-               for _ in range(4)]
-    run_decode_workload(w, 120, samples, check={1, 40, 41, 65, 120})
+               for _ in range(4)] + [(w.layers - 1, w.batch - 1, w.heads - 1)]
+    run_decode_workload(w, steps, samples, check=check, L_cap=max(rows))
