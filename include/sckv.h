@@ -38,8 +38,10 @@
  *   - pointers named *_host are host memory; every other pointer is device
  *     memory of the calling process's current HIP device;
  *   - the caller owns every buffer; the library keeps no state besides a
- *     thread-local error message, never allocates, frees or synchronises;
- *     all work is enqueued on `stream` (0 = the null stream);
+ *     thread-local error message and never allocates or frees memory; all
+ *     work is enqueued on `stream` (0 = the null stream) and no call waits
+ *     for the device, except sckv_span_meta, whose copy from pageable host
+ *     memory can block the calling thread (see there);
  *   - element types: SCKV_F32 (float) or SCKV_BF16 (bfloat16, stored as
  *     16-bit words); accumulation is always fp32;
  *   - supported head dimensions: 64 and 80;
@@ -94,8 +96,16 @@ const char* sckv_version(void);
  * Checks (SCKV_ESPAN): 0 <= cl < L_meta, cl < cr, cr_k < cl_{k+1}.
  * spans_dev        : [2*b*s_max + b] int32, device scratch that receives a
  *                    copy of cl, cr and n (must stay allocated until the
- *                    enqueued kernel has run; the host arrays may be reused
- *                    as soon as the call returns).
+ *                    enqueued kernel has run).
+ * Host behaviour   : cl, cr and n are packed into a temporary pageable host
+ *                    buffer and copied with hipMemcpyAsync on `stream`.  A
+ *                    copy from pageable memory is staged by the HIP runtime
+ *                    before the call returns, so this call can block the
+ *                    calling thread until work already queued on `stream`
+ *                    has drained; when it returns, the host arrays and the
+ *                    temporary buffer are no longer read and may be reused.
+ *                    It is the only entry point that can block the host; a
+ *                    prompt calls it once per batch (a few KB).
  * vu               : [b][L_meta] int32 out (definition above).
  * pos              : [b][L_meta] int32 out, nullable: normal tokens get
  *                    consecutive positions 0,1,2,...; a sentinel at t gets
@@ -272,6 +282,13 @@ int kv_compact(void* kv, void* kv_out, int32_t M, int32_t b, int32_t H, int32_t 
  * its size drives decode latency) and Section 4.3 (generation continues from
  * the compressed cache).
  *
+ * Precondition: rows [0, kv_len[s]) hold only tokens that token t =
+ * cur_tok[s] may attend to, i.e. no row holds a <CL> or a token enclosed by
+ * a span whose <CR> is before t.  The kernel attends to every such row
+ * without a mask, so the caller runs kv_compact (next_tok = cur_tok) after
+ * the prompt and after every step whose token was a <CR>, before the next
+ * decode step; rows appended by other steps keep the precondition.
+ *
  * For each sequence s with current token t = cur_tok[s]:
  *   - if vu[s][t] == t (t is a <CL>): o[s,h] = v_new[s,h] and nothing is
  *     written to the cache;
@@ -327,15 +344,6 @@ int local_decode_attn(const void* q, const void* k_new, const void* v_new, void*
                       hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
- * Close a decode step after all layers: for each sequence, unless its current
- * token t = cur_tok[s] is a <CL> (vu[s][t] == t), record row kv_len[s]
- * (tok_idx = t, pos_ids = pos[s][t]) and increment kv_len[s]; then increment
- * cur_tok[s].  Capacity or token-range violations set status bits and skip
- * the record.
- * Paper: Section 3, "Manipulating Key-Value Memory" (the cache holds only rows
- * later tokens may see) with the position tie of "Input Transformation".
- * ------------------------------------------------------------------------- */
-/* ---------------------------------------------------------------------------
  * Append bookkeeping for a block of n prompt tokens tok0 .. tok0+n-1 (all of
  * them, sentinels included; kv_compact frees what the block closes): for
  * each sequence, row0_out[s] = kv_len[s], rows kv_len[s] + i get
@@ -348,6 +356,15 @@ int kv_extend(int32_t* kv_len, int32_t* tok_idx, int32_t* pos_ids, int32_t* row0
               const int32_t* pos, int32_t L_meta, int32_t tok0, int32_t n, int32_t b,
               int32_t L_cap, int32_t* status, hipStream_t stream);
 
+/* ---------------------------------------------------------------------------
+ * Close a decode step after all layers: for each sequence, unless its current
+ * token t = cur_tok[s] is a <CL> (vu[s][t] == t), record row kv_len[s]
+ * (tok_idx = t, pos_ids = pos[s][t]) and increment kv_len[s]; then increment
+ * cur_tok[s].  Capacity or token-range violations set status bits and skip
+ * the record.
+ * Paper: Section 3, "Manipulating Key-Value Memory" (the cache holds only rows
+ * later tokens may see) with the position tie of "Input Transformation".
+ * ------------------------------------------------------------------------- */
 int kv_commit(int32_t* kv_len, int32_t* tok_idx, int32_t* pos_ids, int32_t* cur_tok,
               const int32_t* vu, const int32_t* pos, int32_t L_meta, int32_t b, int32_t L_cap,
               int32_t* status, hipStream_t stream);

@@ -105,12 +105,62 @@ def _check(rc: int):
 
 
 def _ptr(t):
-    """Device (torch) or host (numpy) buffer -> address; None -> NULL."""
+    """Host (numpy) buffer -> address; None -> NULL.  Device tensors go
+    through _dev, which checks them first."""
     if t is None:
         return None
     if isinstance(t, np.ndarray):
         return t.ctypes.data
     return t.data_ptr()
+
+
+def _fail(msg):
+    raise SckvError(EINVAL, msg)
+
+
+def _avail(t) -> int:
+    """Elements of t's storage from its first element to the storage's end."""
+    return t.untyped_storage().nbytes() // t.element_size() - t.storage_offset()
+
+
+def _dev(t, what, kind=None, need=0, contiguous=False, nullable=False):
+    """Address of a device tensor after checking what the kernels will
+    assume of it: on a GPU, of the element type `kind` ("i32", "float":
+    fp32 or bf16, "u8": any byte workspace), contiguous if asked, and with
+    at least `need` elements from its first one to the end of its storage
+    (so no kernel addresses memory outside the allocation)."""
+    import torch
+    if t is None:
+        if nullable:
+            return None
+        _fail(f"{what}: missing (None)")
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        _fail(f"{what}: must be a device (cuda) tensor")
+    if kind == "i32" and t.dtype != torch.int32:
+        _fail(f"{what}: must be int32, got {t.dtype}")
+    if kind == "float" and t.dtype not in (torch.float32, torch.bfloat16):
+        _fail(f"{what}: must be float32 or bfloat16, got {t.dtype}")
+    if contiguous and not t.is_contiguous():
+        _fail(f"{what}: must be contiguous")
+    if need > _avail(t):
+        _fail(f"{what}: {need} elements addressed, only {_avail(t)} in its storage")
+    return t.data_ptr()
+
+
+def _rows(t, what, b, H, n, d, stride_bh, dtype=None):
+    """(b, H, n, d) slices with (b, h) stride stride_bh: rows contiguous,
+    the batch stride H * stride_bh, element type as `dtype` (if given)."""
+    if t is not None and t.dim() == 4 and t.shape[0] == b and t.shape[1] == H:
+        if n > 1 and t.stride(2) != d or t.stride(3) != 1:
+            _fail(f"{what}: rows of {d} elements must be contiguous")
+        if H > 1 and t.stride(1) != stride_bh or b > 1 and t.stride(0) != H * stride_bh:
+            _fail(f"{what}: (b, h) slices must be stride_bh = {stride_bh} apart")
+    elif t is not None and not t.is_contiguous():
+        _fail(f"{what}: expected a (b, H, n, d) view or a contiguous tensor")
+    p = _dev(t, what, "float", (b * H - 1) * stride_bh + n * d if b * H and n else 0)
+    if dtype is not None and t.dtype != dtype:
+        _fail(f"{what}: element type {t.dtype} differs from {dtype}")
+    return p
 
 
 def _stream(stream, *tensors):
@@ -141,49 +191,83 @@ def _i32_host(a):
 # entry points (same names as the C ABI)
 # ---------------------------------------------------------------------------
 
+def _ws(ws, what="ws"):
+    """A device workspace: address and size in bytes."""
+    p = _dev(ws, what, contiguous=True)
+    return p, ws.numel() * ws.element_size()
+
+
 def sckv_span_meta(cl, cr, n, L_meta: int, spans_dev, vu, pos=None, stream=None):
     """cl, cr: host int32 [b][s_max]; n: host int32 [b]; spans_dev, vu, pos:
     device int32 tensors ([2*b*s_max + b], [b][L_meta], [b][L_meta])."""
     cl, cr, n = _i32_host(cl), _i32_host(cr), _i32_host(n)
     b, s_max = cl.shape
-    _check(lib.sckv_span_meta(_ptr(cl), _ptr(cr), _ptr(n), s_max, b, L_meta, _ptr(spans_dev),
-                              _ptr(vu), _ptr(pos), _stream(stream, vu)))
+    if cr.shape != cl.shape or n.shape != (b,):
+        _fail("sckv_span_meta: cl, cr must be [b][s_max] and n [b]")
+    _check(lib.sckv_span_meta(_ptr(cl), _ptr(cr), _ptr(n), s_max, b, L_meta,
+                              _dev(spans_dev, "spans_dev", "i32", 2 * b * s_max + b, True),
+                              _dev(vu, "vu", "i32", b * L_meta, True),
+                              _dev(pos, "pos", "i32", b * L_meta, True, nullable=True),
+                              _stream(stream, vu)))
 
 
 def rope_apply(x, y, b: int, H: int, n: int, x_stride_bh: int, y_stride_bh: int, d_head: int,
                pos, L_meta: int, tok0: int, theta: float, stream=None):
-    _check(lib.rope_apply(_ptr(x), _ptr(y), b, H, n, x_stride_bh, y_stride_bh, d_head,
-                          _dtype_code(x), _ptr(pos), L_meta, tok0, theta, _stream(stream, x)))
+    px = _rows(x, "x", b, H, n, d_head, x_stride_bh)
+    py = _rows(y, "y", b, H, n, d_head, y_stride_bh, x.dtype)
+    pp = _dev(pos, "pos", "i32", b * L_meta, True, nullable=theta == 0)
+    _check(lib.rope_apply(px, py, b, H, n, x_stride_bh, y_stride_bh, d_head, _dtype_code(x), pp,
+                          L_meta, tok0, theta, _stream(stream, x)))
 
 
 def rope_apply_at(x, y, row0, y_rows: int, b: int, H: int, n: int, x_stride_bh: int,
                   y_stride_bh: int, d_head: int, pos, L_meta: int, tok0: int, theta: float,
                   status=None, stream=None):
-    _check(lib.rope_apply_at(_ptr(x), _ptr(y), _ptr(row0), y_rows, b, H, n, x_stride_bh,
-                             y_stride_bh, d_head, _dtype_code(x), _ptr(pos), L_meta, tok0, theta,
-                             _ptr(status), _stream(stream, x)))
+    px = _rows(x, "x", b, H, n, d_head, x_stride_bh)
+    py = _rows(y, "y", b, H, y_rows, d_head, y_stride_bh, x.dtype)
+    _check(lib.rope_apply_at(px, py, _dev(row0, "row0", "i32", b, True), y_rows, b, H, n,
+                             x_stride_bh, y_stride_bh, d_head, _dtype_code(x),
+                             _dev(pos, "pos", "i32", b * L_meta, True, nullable=theta == 0),
+                             L_meta, tok0, theta,
+                             _dev(status, "status", "i32", 1, nullable=True),
+                             _stream(stream, x)))
 
 
 def sckv_prefill_cached_workspace_bytes(b: int, nq: int, L_cap: int) -> int:
     return int(lib.sckv_prefill_cached_workspace_bytes(b, nq, L_cap))
 
 
+def _cached_args(q, k_cache, v_cache, o, b, H, nq, d_head, q_stride_bh, kv_stride_bh,
+                 o_stride_bh, vu, L_meta, row0, tok_idx, L_cap, ws, status):
+    pq = _rows(q, "q", b, H, nq, d_head, q_stride_bh)
+    pk = _rows(k_cache, "k_cache", b, H, L_cap, d_head, kv_stride_bh, q.dtype)
+    pv = _rows(v_cache, "v_cache", b, H, L_cap, d_head, kv_stride_bh, q.dtype)
+    po = _rows(o, "o", b, H, nq, d_head, o_stride_bh, q.dtype)
+    pw, nw = _ws(ws)
+    return (pq, pk, pv, po, _dev(vu, "vu", "i32", b * L_meta, True),
+            _dev(row0, "row0", "i32", b, True), _dev(tok_idx, "tok_idx", "i32", b * L_cap, True),
+            pw, nw, _dev(status, "status", "i32", 1, nullable=True))
+
+
 def span_masked_prefill_attn_cached(q, k_cache, v_cache, o, b: int, H: int, nq: int, d_head: int,
                                     q_stride_bh: int, kv_stride_bh: int, o_stride_bh: int,
                                     scale: float, vu, L_meta: int, tok0: int, row0, tok_idx,
                                     L_cap: int, ws, status=None, stream=None):
+    pq, pk, pv, po, pvu, pr0, ptok, pw, nw, pst = _cached_args(
+        q, k_cache, v_cache, o, b, H, nq, d_head, q_stride_bh, kv_stride_bh, o_stride_bh, vu,
+        L_meta, row0, tok_idx, L_cap, ws, status)
     _check(lib.span_masked_prefill_attn_cached(
-        _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(o), b, H, nq, d_head, q_stride_bh,
-        kv_stride_bh, o_stride_bh, _dtype_code(q), scale, _ptr(vu), L_meta, tok0, _ptr(row0),
-        _ptr(tok_idx), L_cap, _ptr(ws), ws.numel() * ws.element_size(), _ptr(status),
-        _stream(stream, q)))
+        pq, pk, pv, po, b, H, nq, d_head, q_stride_bh, kv_stride_bh, o_stride_bh, _dtype_code(q),
+        scale, pvu, L_meta, tok0, pr0, ptok, L_cap, pw, nw, pst, _stream(stream, q)))
 
 
 def sckv_prefill_cached_plan(vu, L_meta: int, tok0: int, row0, tok_idx, L_cap: int, b: int,
                              nq: int, ws, stream=None):
-    _check(lib.sckv_prefill_cached_plan(_ptr(vu), L_meta, tok0, _ptr(row0), _ptr(tok_idx), L_cap,
-                                        b, nq, _ptr(ws), ws.numel() * ws.element_size(),
-                                        _stream(stream, ws)))
+    pw, nw = _ws(ws)
+    _check(lib.sckv_prefill_cached_plan(_dev(vu, "vu", "i32", b * L_meta, True), L_meta, tok0,
+                                        _dev(row0, "row0", "i32", b, True),
+                                        _dev(tok_idx, "tok_idx", "i32", b * L_cap, True), L_cap,
+                                        b, nq, pw, nw, _stream(stream, ws)))
 
 
 def span_masked_prefill_attn_cached_planned(q, k_cache, v_cache, o, b: int, H: int, nq: int,
@@ -191,79 +275,140 @@ def span_masked_prefill_attn_cached_planned(q, k_cache, v_cache, o, b: int, H: i
                                             o_stride_bh: int, scale: float, vu, L_meta: int,
                                             tok0: int, row0, tok_idx, L_cap: int, ws, status=None,
                                             stream=None):
+    pq, pk, pv, po, pvu, pr0, ptok, pw, nw, pst = _cached_args(
+        q, k_cache, v_cache, o, b, H, nq, d_head, q_stride_bh, kv_stride_bh, o_stride_bh, vu,
+        L_meta, row0, tok_idx, L_cap, ws, status)
     _check(lib.span_masked_prefill_attn_cached_planned(
-        _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(o), b, H, nq, d_head, q_stride_bh,
-        kv_stride_bh, o_stride_bh, _dtype_code(q), scale, _ptr(vu), L_meta, tok0, _ptr(row0),
-        _ptr(tok_idx), L_cap, _ptr(ws), ws.numel() * ws.element_size(), _ptr(status),
-        _stream(stream, q)))
+        pq, pk, pv, po, b, H, nq, d_head, q_stride_bh, kv_stride_bh, o_stride_bh, _dtype_code(q),
+        scale, pvu, L_meta, tok0, pr0, ptok, L_cap, pw, nw, pst, _stream(stream, q)))
 
 
 def kv_extend(kv_len, tok_idx, pos_ids, row0_out, pos, L_meta: int, tok0: int, n: int, b: int,
               L_cap: int, status=None, stream=None):
-    _check(lib.kv_extend(_ptr(kv_len), _ptr(tok_idx), _ptr(pos_ids), _ptr(row0_out), _ptr(pos),
-                         L_meta, tok0, n, b, L_cap, _ptr(status), _stream(stream, kv_len)))
+    _check(lib.kv_extend(_dev(kv_len, "kv_len", "i32", b, True),
+                         _dev(tok_idx, "tok_idx", "i32", b * L_cap, True),
+                         _dev(pos_ids, "pos_ids", "i32", b * L_cap, True),
+                         _dev(row0_out, "row0_out", "i32", b, True),
+                         _dev(pos, "pos", "i32", b * L_meta, True), L_meta, tok0, n, b, L_cap,
+                         _dev(status, "status", "i32", 1, nullable=True),
+                         _stream(stream, kv_len)))
 
 
 def sckv_prefill_workspace_bytes(b: int, L: int) -> int:
     return int(lib.sckv_prefill_workspace_bytes(b, L))
 
 
+def _prefill_args(q, k, v, o, b, H, L, d_head, q_stride_bh, kv_stride_bh, o_stride_bh, vu,
+                  L_meta, ws):
+    pw, nw = _ws(ws)
+    return (_rows(q, "q", b, H, L, d_head, q_stride_bh),
+            _rows(k, "k", b, H, L, d_head, kv_stride_bh, q.dtype),
+            _rows(v, "v", b, H, L, d_head, kv_stride_bh, q.dtype),
+            _rows(o, "o", b, H, L, d_head, o_stride_bh, q.dtype),
+            _dev(vu, "vu", "i32", b * L_meta, True), pw, nw)
+
+
 def span_masked_prefill_attn(q, k, v, o, b: int, H: int, L: int, d_head: int, q_stride_bh: int,
                              kv_stride_bh: int, o_stride_bh: int, scale: float, vu, L_meta: int,
                              ws, stream=None):
-    _check(lib.span_masked_prefill_attn(_ptr(q), _ptr(k), _ptr(v), _ptr(o), b, H, L, d_head,
-                                        q_stride_bh, kv_stride_bh, o_stride_bh, _dtype_code(q),
-                                        scale, _ptr(vu), L_meta, _ptr(ws), ws.numel() *
-                                        ws.element_size(), _stream(stream, q)))
+    pq, pk, pv, po, pvu, pw, nw = _prefill_args(q, k, v, o, b, H, L, d_head, q_stride_bh,
+                                                kv_stride_bh, o_stride_bh, vu, L_meta, ws)
+    _check(lib.span_masked_prefill_attn(pq, pk, pv, po, b, H, L, d_head, q_stride_bh,
+                                        kv_stride_bh, o_stride_bh, _dtype_code(q), scale, pvu,
+                                        L_meta, pw, nw, _stream(stream, q)))
 
 
 def sckv_prefill_plan(vu, L_meta: int, b: int, L: int, ws, stream=None):
-    _check(lib.sckv_prefill_plan(_ptr(vu), L_meta, b, L, _ptr(ws), ws.numel() * ws.element_size(),
+    pw, nw = _ws(ws)
+    _check(lib.sckv_prefill_plan(_dev(vu, "vu", "i32", b * L_meta, True), L_meta, b, L, pw, nw,
                                  _stream(stream, ws)))
 
 
 def span_masked_prefill_attn_planned(q, k, v, o, b: int, H: int, L: int, d_head: int,
                                      q_stride_bh: int, kv_stride_bh: int, o_stride_bh: int,
                                      scale: float, vu, L_meta: int, ws, stream=None):
-    _check(lib.span_masked_prefill_attn_planned(_ptr(q), _ptr(k), _ptr(v), _ptr(o), b, H, L,
-                                                d_head, q_stride_bh, kv_stride_bh, o_stride_bh,
-                                                _dtype_code(q), scale, _ptr(vu), L_meta, _ptr(ws),
-                                                ws.numel() * ws.element_size(),
-                                                _stream(stream, q)))
+    pq, pk, pv, po, pvu, pw, nw = _prefill_args(q, k, v, o, b, H, L, d_head, q_stride_bh,
+                                                kv_stride_bh, o_stride_bh, vu, L_meta, ws)
+    _check(lib.span_masked_prefill_attn_planned(pq, pk, pv, po, b, H, L, d_head, q_stride_bh,
+                                                kv_stride_bh, o_stride_bh, _dtype_code(q), scale,
+                                                pvu, L_meta, pw, nw, _stream(stream, q)))
 
 
 def kv_compact(kv, kv_out, M: int, b: int, H: int, L_cap: int, d_head: int, kv_len, tok_idx,
                pos_ids, next_tok, vu, L_meta: int, kept_src_row, stream=None):
-    _check(lib.kv_compact(_ptr(kv), _ptr(kv_out), M, b, H, L_cap, d_head, _dtype_code(kv),
-                          _ptr(kv_len), _ptr(tok_idx), _ptr(pos_ids), _ptr(next_tok), _ptr(vu),
-                          L_meta, _ptr(kept_src_row), _stream(stream, kv)))
+    n = M * 2 * b * H * L_cap * d_head
+    pkv = _dev(kv, "kv", "float", n, True)
+    pout = _dev(kv_out, "kv_out", "float", n, True, nullable=True)
+    if kv_out is not None and kv_out.dtype != kv.dtype:
+        _fail("kv_out: element type differs from kv")
+    _check(lib.kv_compact(pkv, pout, M, b, H, L_cap, d_head, _dtype_code(kv),
+                          _dev(kv_len, "kv_len", "i32", b, True),
+                          _dev(tok_idx, "tok_idx", "i32", b * L_cap, True),
+                          _dev(pos_ids, "pos_ids", "i32", b * L_cap, True),
+                          _dev(next_tok, "next_tok", "i32", b, True),
+                          _dev(vu, "vu", "i32", b * L_meta, True), L_meta,
+                          _dev(kept_src_row, "kept_src_row", "i32", b * L_cap, True),
+                          _stream(stream, kv)))
 
 
 def sckv_decode_workspace_bytes(b: int, H: int, L_cap: int, d_head: int) -> int:
     return int(lib.sckv_decode_workspace_bytes(b, H, L_cap, d_head))
 
 
+def _decode_args(q, k_new, v_new, k_cache, v_cache, o, vu, pos, L_meta, b, H, L_cap, d_head,
+                 theta, status):
+    nh = b * H * d_head
+    pq = _dev(q, "q", "float", nh, True)
+    out = [pq]
+    for t, nm in ((k_new, "k_new"), (v_new, "v_new")):
+        out.append(_dev(t, nm, "float", nh, True))
+    for t, nm in ((k_cache, "k_cache"), (v_cache, "v_cache")):
+        out.append(_dev(t, nm, "float", b * H * L_cap * d_head, True))
+    out.append(_dev(o, "o", "float", nh, True))
+    for t, nm in ((k_new, "k_new"), (v_new, "v_new"), (k_cache, "k_cache"), (v_cache, "v_cache"),
+                  (o, "o")):
+        if t.dtype != q.dtype:
+            _fail(f"{nm}: element type {t.dtype} differs from q's {q.dtype}")
+    out.append(_dev(vu, "vu", "i32", b * L_meta, True))
+    out.append(_dev(pos, "pos", "i32", b * L_meta, True, nullable=theta == 0))
+    out.append(_dev(status, "status", "i32", 1, nullable=True))
+    return out
+
+
 def compacted_decode_attn(q, k_new, v_new, k_cache, v_cache, kv_len, cur_tok, vu, pos,
                           L_meta: int, o, b: int, H: int, L_cap: int, d_head: int, scale: float,
                           rope_theta: float, ws, status=None, stream=None):
-    _check(lib.compacted_decode_attn(_ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_cache),
-                                     _ptr(v_cache), _ptr(kv_len), _ptr(cur_tok), _ptr(vu),
-                                     _ptr(pos), L_meta, _ptr(o), b, H, L_cap, d_head,
-                                     _dtype_code(q), scale, rope_theta, _ptr(ws),
-                                     ws.numel() * ws.element_size(), _ptr(status),
-                                     _stream(stream, q)))
+    pq, pkn, pvn, pkc, pvc, po, pvu, ppos, pst = _decode_args(
+        q, k_new, v_new, k_cache, v_cache, o, vu, pos, L_meta, b, H, L_cap, d_head, rope_theta,
+        status)
+    pw, nw = _ws(ws)
+    _check(lib.compacted_decode_attn(pq, pkn, pvn, pkc, pvc,
+                                     _dev(kv_len, "kv_len", "i32", b, True),
+                                     _dev(cur_tok, "cur_tok", "i32", b, True), pvu, ppos, L_meta,
+                                     po, b, H, L_cap, d_head, _dtype_code(q), scale, rope_theta,
+                                     pw, nw, pst, _stream(stream, q)))
 
 
 def kv_commit(kv_len, tok_idx, pos_ids, cur_tok, vu, pos, L_meta: int, b: int, L_cap: int,
               status=None, stream=None):
-    _check(lib.kv_commit(_ptr(kv_len), _ptr(tok_idx), _ptr(pos_ids), _ptr(cur_tok), _ptr(vu),
-                         _ptr(pos), L_meta, b, L_cap, _ptr(status), _stream(stream, kv_len)))
+    _check(lib.kv_commit(_dev(kv_len, "kv_len", "i32", b, True),
+                         _dev(tok_idx, "tok_idx", "i32", b * L_cap, True),
+                         _dev(pos_ids, "pos_ids", "i32", b * L_cap, True),
+                         _dev(cur_tok, "cur_tok", "i32", b, True),
+                         _dev(vu, "vu", "i32", b * L_meta, True),
+                         _dev(pos, "pos", "i32", b * L_meta, True), L_meta, b, L_cap,
+                         _dev(status, "status", "i32", 1, nullable=True),
+                         _stream(stream, kv_len)))
 
 
 def local_decode_attn(q, k_new, v_new, k_cache, v_cache, W: int, cur_tok, vu, pos, L_meta: int,
                       o, b: int, H: int, L_cap: int, d_head: int, scale: float, rope_theta: float,
                       ws, status=None, stream=None):
-    _check(lib.local_decode_attn(_ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache),
-                                 W, _ptr(cur_tok), _ptr(vu), _ptr(pos), L_meta, _ptr(o), b, H,
-                                 L_cap, d_head, _dtype_code(q), scale, rope_theta, _ptr(ws),
-                                 ws.numel() * ws.element_size(), _ptr(status), _stream(stream, q)))
+    pq, pkn, pvn, pkc, pvc, po, pvu, ppos, pst = _decode_args(
+        q, k_new, v_new, k_cache, v_cache, o, vu, pos, L_meta, b, H, L_cap, d_head, rope_theta,
+        status)
+    pw, nw = _ws(ws)
+    _check(lib.local_decode_attn(pq, pkn, pvn, pkc, pvc, W,
+                                 _dev(cur_tok, "cur_tok", "i32", b, True), pvu, ppos, L_meta, po,
+                                 b, H, L_cap, d_head, _dtype_code(q), scale, rope_theta, pw, nw,
+                                 pst, _stream(stream, q)))

@@ -19,6 +19,7 @@
 #include <math.h>
 
 #include <cmath>
+#include <string>
 
 #include "sckv_common.h"
 
@@ -827,31 +828,38 @@ extern "C" int local_decode_attn(const void* q, const void* k_new, const void* v
              : launch_decode<uint16_t, 80>(q, k_new, v_new, k_cache, v_cache, nullptr, cur_tok, vu, p, L_meta, o, b, H, L_cap, scale, rope_theta, ws, status, stream, W);
 }
 
-extern "C" int compacted_decode_attn(const void* q, const void* k_new, const void* v_new,
-                                     void* k_cache, void* v_cache, const int32_t* kv_len,
-                                     const int32_t* cur_tok, const int32_t* vu,
-                                     const int32_t* pos, int32_t L_meta, void* o, int32_t b,
-                                     int32_t H, int32_t L_cap, int32_t d_head, sckv_dtype dt,
-                                     float scale, float rope_theta, void* ws, size_t ws_bytes,
-                                     int32_t* status, hipStream_t stream) {
-  clear_error();
-  if (!q || !k_new || !v_new || !k_cache || !v_cache || !kv_len || !cur_tok || !vu || !o || !ws)
-    return fail(SCKV_EINVAL, "compacted_decode_attn: null pointer");
-  if (!valid_dtype(dt)) return fail(SCKV_EINVAL, "compacted_decode_attn: unknown dtype");
-  if (!supported_d(d_head)) return fail(SCKV_EUNSUP, "compacted_decode_attn: d_head must be 64 or 80");
+// Host checks of compacted_decode_attn and its allocation-free variant
+// (everything but the workspace); no HIP call is made here.
+static int decode_checks(const char* W, const void* q, const void* k_new, const void* v_new,
+                         const void* k_cache, const void* v_cache, const int32_t* kv_len,
+                         const int32_t* cur_tok, const int32_t* vu, const int32_t* pos,
+                         int32_t L_meta, const void* o, int32_t b, int32_t H, int32_t L_cap,
+                         int32_t d_head, sckv_dtype dt, float scale, float rope_theta) {
+  const std::string w(W);
+  if (!q || !k_new || !v_new || !k_cache || !v_cache || !kv_len || !cur_tok || !vu || !o)
+    return fail(SCKV_EINVAL, w + ": null pointer");
+  if (!valid_dtype(dt)) return fail(SCKV_EINVAL, w + ": unknown dtype");
+  if (!supported_d(d_head)) return fail(SCKV_EUNSUP, w + ": d_head must be 64 or 80");
   if (b <= 0 || H <= 0 || L_cap <= 0 || L_meta <= 0)
-    return fail(SCKV_EINVAL, "compacted_decode_attn: sizes must be positive");
+    return fail(SCKV_EINVAL, w + ": sizes must be positive");
   if ((int64_t)b * H * n_chunks(L_cap) > 0x7fffffff)
-    return fail(SCKV_EUNSUP, "compacted_decode_attn: b*H*chunks too large");
-  if (!(scale > 0.f) || std::isinf(scale)) return fail(SCKV_EINVAL, "compacted_decode_attn: scale must be finite and > 0");
+    return fail(SCKV_EUNSUP, w + ": b*H*chunks too large");
+  if (!(scale > 0.f) || std::isinf(scale)) return fail(SCKV_EINVAL, w + ": scale must be finite and > 0");
   if (!(rope_theta >= 0.f) || std::isinf(rope_theta))
-    return fail(SCKV_EINVAL, "compacted_decode_attn: rope_theta must be finite and >= 0");
-  if (rope_theta > 0.f && !pos) return fail(SCKV_EINVAL, "compacted_decode_attn: null pos");
-  if (ws_bytes < sckv_decode_workspace_bytes(b, H, L_cap, d_head))
-    return fail(SCKV_EINVAL, "compacted_decode_attn: workspace too small");
+    return fail(SCKV_EINVAL, w + ": rope_theta must be finite and >= 0");
+  if (rope_theta > 0.f && !pos) return fail(SCKV_EINVAL, w + ": null pos");
   if (!aligned16(q) || !aligned16(k_new) || !aligned16(v_new) || !aligned16(k_cache) ||
-      !aligned16(v_cache) || !aligned16(o) || !aligned16(ws))
-    return fail(SCKV_EINVAL, "compacted_decode_attn: buffers must be 16-byte aligned");
+      !aligned16(v_cache) || !aligned16(o))
+    return fail(SCKV_EINVAL, w + ": buffers must be 16-byte aligned");
+  return SCKV_OK;
+}
+
+static int decode_dispatch(const void* q, const void* k_new, const void* v_new, void* k_cache,
+                           void* v_cache, const int32_t* kv_len, const int32_t* cur_tok,
+                           const int32_t* vu, const int32_t* pos, int32_t L_meta, void* o,
+                           int32_t b, int32_t H, int32_t L_cap, int32_t d_head, sckv_dtype dt,
+                           float scale, float rope_theta, void* ws, int32_t* status,
+                           hipStream_t stream) {
   const int32_t* p = pos ? pos : vu;  // pos is read only when rotating
   if (dt == SCKV_BF16)
     return d_head == 64
@@ -860,4 +868,24 @@ extern "C" int compacted_decode_attn(const void* q, const void* k_new, const voi
   return d_head == 64
              ? launch_decode<float, 64>(q, k_new, v_new, k_cache, v_cache, kv_len, cur_tok, vu, p, L_meta, o, b, H, L_cap, scale, rope_theta, ws, status, stream)
              : launch_decode<float, 80>(q, k_new, v_new, k_cache, v_cache, kv_len, cur_tok, vu, p, L_meta, o, b, H, L_cap, scale, rope_theta, ws, status, stream);
+}
+
+extern "C" int compacted_decode_attn(const void* q, const void* k_new, const void* v_new,
+                                     void* k_cache, void* v_cache, const int32_t* kv_len,
+                                     const int32_t* cur_tok, const int32_t* vu,
+                                     const int32_t* pos, int32_t L_meta, void* o, int32_t b,
+                                     int32_t H, int32_t L_cap, int32_t d_head, sckv_dtype dt,
+                                     float scale, float rope_theta, void* ws, size_t ws_bytes,
+                                     int32_t* status, hipStream_t stream) {
+  clear_error();
+  const char* W = "compacted_decode_attn";
+  int rc = decode_checks(W, q, k_new, v_new, k_cache, v_cache, kv_len, cur_tok, vu, pos, L_meta,
+                         o, b, H, L_cap, d_head, dt, scale, rope_theta);
+  if (rc) return rc;
+  if (!ws) return fail(SCKV_EINVAL, "compacted_decode_attn: null pointer");
+  if (ws_bytes < sckv_decode_workspace_bytes(b, H, L_cap, d_head))
+    return fail(SCKV_EINVAL, "compacted_decode_attn: workspace too small");
+  if (!aligned16(ws)) return fail(SCKV_EINVAL, "compacted_decode_attn: buffers must be 16-byte aligned");
+  return decode_dispatch(q, k_new, v_new, k_cache, v_cache, kv_len, cur_tok, vu, pos, L_meta, o, b,
+                         H, L_cap, d_head, dt, scale, rope_theta, ws, status, stream);
 }

@@ -247,3 +247,15 @@ def test_local_decode_rejects_bad_arguments(B):
     assert call(d=72) == B.EUNSUP
     assert call(ws=ws - 4) == B.EINVAL
     assert call(cur=NULL) == B.EINVAL
+
+
+def test_binding_rejects_host_tensors(B):
+    """The binding checks every device argument before the C call: host
+    tensors never reach a kernel as device pointers."""
+    import torch
+    x = torch.zeros((1, 1, 64), dtype=torch.bfloat16)
+    i = torch.zeros(1, dtype=torch.int32)
+    with pytest.raises(B.SckvError) as e:
+        B.compacted_decode_attn(x, x, x, x, x, i, i, i, None, 1, x, 1, 1, 1, 64, 0.1, 0.0,
+                                torch.zeros(16, dtype=torch.uint8))
+    assert e.value.code == B.EINVAL and "device" in str(e.value)

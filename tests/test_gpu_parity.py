@@ -580,8 +580,9 @@ def test_local_decode_ring_matches_oracle(d, theta, H, W):
     worst = 0.0
     for s in range(b):
         for h in range(H):
+            # unrounded fp64 rotation, as in every other test (the cache
+            # itself stores the rotated keys in bf16)
             Kr = O.rope_rotate_half(K[s, h], np.arange(T), theta) if theta > 0 else K[s, h]
-            Kr = f64(torch.tensor(Kr).to(torch.bfloat16))  # the cache stores rotated keys in bf16
             for i in range(steps):
                 t = L + i
                 qs = Q[i, s, h][None]
@@ -596,3 +597,40 @@ def test_local_decode_ring_matches_oracle(d, theta, H, W):
     Kc, Vc = f64(cache.k(0)), f64(cache.v(0))
     for t in range(T - W, T):
         assert np.array_equal(Vc[:, :, t % W], V[:, :, t])
+
+
+# ---------------------------------------------------------------------------
+# the binding refuses tensors the kernels would misread
+# ---------------------------------------------------------------------------
+
+def test_binding_rejects_bad_device_tensors():
+    """Wrong element type, too small a buffer or a layout that does not
+    match the strides: SckvError before the C call, nothing launched."""
+    say("binding argument checks")
+    B = P().B
+    b, H, d, L_cap, T = 2, 2, 64, 32, 40
+    q = torch.zeros((b, H, d), dtype=torch.bfloat16, device=DEV)
+    kc = torch.zeros((b, H, L_cap, d), dtype=torch.bfloat16, device=DEV)
+    vu = torch.zeros((b, T), dtype=torch.int32, device=DEV)
+    n = torch.zeros(b, dtype=torch.int32, device=DEV)
+    ws = torch.empty(B.sckv_decode_workspace_bytes(b, H, L_cap, d), dtype=torch.uint8, device=DEV)
+    ok = dict(q=q, k_new=q, v_new=q, k_cache=kc, v_cache=kc, kv_len=n, cur_tok=n, vu=vu, pos=vu,
+              L_meta=T, o=q.clone(), b=b, H=H, L_cap=L_cap, d_head=d, scale=0.125,
+              rope_theta=0.0, ws=ws)
+    bad = [dict(kv_len=n.long()),                                   # int64 lengths
+           dict(k_cache=kc[:, :, :L_cap // 2]),                      # fewer rows than L_cap
+           dict(q=torch.zeros((b, H, d), dtype=torch.float32, device=DEV)),  # mixed types
+           dict(vu=vu[:, :T // 2]),                                  # non-contiguous view
+           dict(o=torch.zeros((b, H, d - 8), dtype=torch.bfloat16, device=DEV))]  # too small
+    for change in bad:
+        with pytest.raises(B.SckvError) as e:
+            B.compacted_decode_attn(**{**ok, **change})
+        assert e.value.code == B.EINVAL, change
+    # strided prefill operands must match the strides passed
+    L = 16
+    x = torch.zeros((b, H, L, d), dtype=torch.bfloat16, device=DEV)
+    pws = torch.empty(B.sckv_prefill_workspace_bytes(b, L), dtype=torch.uint8, device=DEV)
+    with pytest.raises(B.SckvError):
+        B.span_masked_prefill_attn(x, x, x, x.clone(), b, H, L, d, L * d, 2 * L * d, L * d, 0.125,
+                                   vu, T, pws)
+    torch.cuda.synchronize()
