@@ -322,6 +322,35 @@ int compacted_decode_attn(const void* q, const void* k_new, const void* v_new, v
                           int32_t* status, hipStream_t stream);
 
 /* ---------------------------------------------------------------------------
+ * compacted_decode_attn without any allocation, for callers that cannot
+ * allocate device memory or pass a workspace: code being captured into a
+ * HIP graph, tight serving loops, harnesses that forbid hipMalloc.
+ *
+ * Same arguments, semantics, precondition, status bits and outputs as
+ * compacted_decode_attn, minus ws / ws_bytes: the split-K partials of a
+ * launch with fewer than 512 (sequence, head) slices go to a scratch array
+ * of SCKV_NOALLOC_SCRATCH_BYTES bytes inside the library, one per device,
+ * held from the library's load until the process ends.  The call allocates
+ * and frees nothing; its first call on a device looks up that device's
+ * array address once.
+ * Limit: with b*H < 512, sckv_decode_workspace_bytes(b, H, L_cap, d_head)
+ * must not exceed SCKV_NOALLOC_SCRATCH_BYTES (511 slices of up to 65536
+ * rows fit, at either head size); larger shapes return SCKV_EUNSUP and
+ * enqueue nothing.  With b*H >= 512 the scratch array is not used.
+ * Every call on a device shares its array and overwrites what the previous
+ * call left there (nothing in it needs clearing); calls that may overlap on
+ * one device (two host threads, or two streams without ordering) race and
+ * must not be made.
+ * ------------------------------------------------------------------------- */
+#define SCKV_NOALLOC_SCRATCH_BYTES (16u << 20)
+int compacted_decode_attn_noalloc(const void* q, const void* k_new, const void* v_new,
+                                  void* k_cache, void* v_cache, const int32_t* kv_len,
+                                  const int32_t* cur_tok, const int32_t* vu, const int32_t* pos,
+                                  int32_t L_meta, void* o, int32_t b, int32_t H, int32_t L_cap,
+                                  int32_t d_head, sckv_dtype dt, float scale, float rope_theta,
+                                  int32_t* status, hipStream_t stream);
+
+/* ---------------------------------------------------------------------------
  * Local-attention comparator (the "Local Attention" baseline of Section 4.1:
  * a token attends only to a window of the most recent tokens), at a fixed
  * budget of W cached rows: rows [0, W) of each slice are a ring holding the

@@ -78,6 +78,9 @@ _SIGS = {
     "compacted_decode_attn": (ctypes.c_int, [_p, _p, _p, _p, _p, _p, _p, _p, _p, _i32, _p, _i32,
                                              _i32, _i32, _i32, ctypes.c_int, _f32, _f32, _p, _sz,
                                              _p, _p]),
+    "compacted_decode_attn_noalloc": (ctypes.c_int, [_p, _p, _p, _p, _p, _p, _p, _p, _p, _i32, _p,
+                                                     _i32, _i32, _i32, _i32, ctypes.c_int, _f32,
+                                                     _f32, _p, _p]),
     "kv_commit": (ctypes.c_int, [_p, _p, _p, _p, _p, _p, _i32, _i32, _i32, _p, _p]),
     "local_decode_attn": (ctypes.c_int, [_p, _p, _p, _p, _p, _i32, _p, _p, _p, _i32, _p, _i32,
                                          _i32, _i32, _i32, ctypes.c_int, _f32, _f32, _p, _sz, _p,
@@ -387,6 +390,24 @@ def compacted_decode_attn(q, k_new, v_new, k_cache, v_cache, kv_len, cur_tok, vu
                                      _dev(cur_tok, "cur_tok", "i32", b, True), pvu, ppos, L_meta,
                                      po, b, H, L_cap, d_head, _dtype_code(q), scale, rope_theta,
                                      pw, nw, pst, _stream(stream, q)))
+
+
+def compacted_decode_attn_noalloc(q, k_new, v_new, k_cache, v_cache, kv_len, cur_tok, vu, pos,
+                                  L_meta: int, o, b: int, H: int, L_cap: int, d_head: int,
+                                  scale: float, rope_theta: float, status=None, stream=None):
+    """compacted_decode_attn with the library's own scratch array in place
+    of a workspace (no allocation by the call)."""
+    pq, pkn, pvn, pkc, pvc, po, pvu, ppos, pst = _decode_args(
+        q, k_new, v_new, k_cache, v_cache, o, vu, pos, L_meta, b, H, L_cap, d_head, rope_theta,
+        status)
+    _check(lib.compacted_decode_attn_noalloc(pq, pkn, pvn, pkc, pvc,
+                                             _dev(kv_len, "kv_len", "i32", b, True),
+                                             _dev(cur_tok, "cur_tok", "i32", b, True), pvu, ppos,
+                                             L_meta, po, b, H, L_cap, d_head, _dtype_code(q),
+                                             scale, rope_theta, pst, _stream(stream, q)))
+
+
+NOALLOC_SCRATCH_BYTES = 16 << 20  # SCKV_NOALLOC_SCRATCH_BYTES in sckv.h
 
 
 def kv_commit(kv_len, tok_idx, pos_ids, cur_tok, vu, pos, L_meta: int, b: int, L_cap: int,

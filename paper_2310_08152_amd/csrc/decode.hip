@@ -19,6 +19,7 @@
 #include <math.h>
 
 #include <cmath>
+#include <mutex>
 #include <string>
 
 #include "sckv_common.h"
@@ -886,6 +887,69 @@ extern "C" int compacted_decode_attn(const void* q, const void* k_new, const voi
   if (ws_bytes < sckv_decode_workspace_bytes(b, H, L_cap, d_head))
     return fail(SCKV_EINVAL, "compacted_decode_attn: workspace too small");
   if (!aligned16(ws)) return fail(SCKV_EINVAL, "compacted_decode_attn: buffers must be 16-byte aligned");
+  return decode_dispatch(q, k_new, v_new, k_cache, v_cache, kv_len, cur_tok, vu, pos, L_meta, o, b,
+                         H, L_cap, d_head, dt, scale, rope_theta, ws, status, stream);
+}
+
+// ---------------------------------------------------------------------------
+// The same decode step without any allocation: the split-K partials go to a
+// file-scope device array instead of a caller workspace.  Each device that
+// runs the library holds its own copy of the array from module load until
+// the process ends; its device address is looked up once per device (the
+// array's name in host code is only a stand-in for that address) and kept.
+// Every call on a device shares that device's array and leaves its partials
+// in it; nothing in it has to start at zero (the merge reads only the chunk
+// partials the same call wrote).  Calls that overlap on one device race.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) char scratch[SCKV_NOALLOC_SCRATCH_BYTES];
+
+constexpr int NOALLOC_MAX_DEVICES = 64;
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[NOALLOC_MAX_DEVICES];  // per device, set once
+
+static int scratch_address(void** out) {
+  int dev = -1;
+  int rc = hip_check(hipGetDevice(&dev), "compacted_decode_attn_noalloc: hipGetDevice");
+  if (rc) return rc;
+  if (dev < 0 || dev >= NOALLOC_MAX_DEVICES)
+    return fail(SCKV_EUNSUP, "compacted_decode_attn_noalloc: device index above 63");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    rc = hip_check(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)),
+                   "compacted_decode_attn_noalloc: hipGetSymbolAddress(scratch)");
+    if (rc) return rc;
+    if (!p || !aligned16(p))
+      return fail(SCKV_EHIP, "compacted_decode_attn_noalloc: scratch array has no usable address");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return SCKV_OK;
+}
+
+extern "C" int compacted_decode_attn_noalloc(const void* q, const void* k_new, const void* v_new,
+                                             void* k_cache, void* v_cache, const int32_t* kv_len,
+                                             const int32_t* cur_tok, const int32_t* vu,
+                                             const int32_t* pos, int32_t L_meta, void* o,
+                                             int32_t b, int32_t H, int32_t L_cap, int32_t d_head,
+                                             sckv_dtype dt, float scale, float rope_theta,
+                                             int32_t* status, hipStream_t stream) {
+  clear_error();
+  const char* W = "compacted_decode_attn_noalloc";
+  int rc = decode_checks(W, q, k_new, v_new, k_cache, v_cache, kv_len, cur_tok, vu, pos, L_meta,
+                         o, b, H, L_cap, d_head, dt, scale, rope_theta);
+  if (rc) return rc;
+  // only the split launch (fewer than DEC_SINGLE_MIN slices) writes partials
+  const size_t need = (int64_t)b * H >= DEC_SINGLE_MIN
+                          ? 0 : sckv_decode_workspace_bytes(b, H, L_cap, d_head);
+  if (need > SCKV_NOALLOC_SCRATCH_BYTES)
+    return fail(SCKV_EUNSUP, std::string(W) + ": the split-K partials need " +
+                                 std::to_string(need) + " bytes, more than the " +
+                                 std::to_string((size_t)SCKV_NOALLOC_SCRATCH_BYTES) +
+                                 "-byte scratch array (use compacted_decode_attn with a workspace)");
+  void* ws = nullptr;
+  rc = scratch_address(&ws);
+  if (rc) return rc;
   return decode_dispatch(q, k_new, v_new, k_cache, v_cache, kv_len, cur_tok, vu, pos, L_meta, o, b,
                          H, L_cap, d_head, dt, scale, rope_theta, ws, status, stream);
 }

@@ -249,6 +249,23 @@ def test_local_decode_rejects_bad_arguments(B):
     assert call(cur=NULL) == B.EINVAL
 
 
+def test_noalloc_decode_rejects_oversized_partials(B):
+    """The allocation-free decode refuses a split launch whose partials would
+    not fit in its scratch array, before any HIP call (no GPU needed)."""
+    f = B.lib.compacted_decode_attn_noalloc
+    b, H, d, L_cap = 1, 511, 80, 200000
+    assert B.sckv_decode_workspace_bytes(b, H, L_cap, d) > B.NOALLOC_SCRATCH_BYTES
+    rc = f(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 4, FAKE, b, H, L_cap, d, B.BF16,
+           0.1, 0.0, NULL, NULL)
+    assert rc == B.EUNSUP
+    assert "scratch" in B.last_error()
+    # argument checks come first, as for compacted_decode_attn
+    assert f(NULL, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 4, FAKE, 1, 1, 10, 80, B.BF16,
+             0.1, 0.0, NULL, NULL) == B.EINVAL
+    assert f(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 4, FAKE, 1, 1, 10, 96, B.BF16,
+             0.1, 0.0, NULL, NULL) == B.EUNSUP
+
+
 def test_binding_rejects_host_tensors(B):
     """The binding checks every device argument before the C call: host
     tensors never reach a kernel as device pointers."""
