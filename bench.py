@@ -15,7 +15,16 @@ synthetic N(0,1) bf16 tensors resident in HBM before timing starts.
 
 value = compacted-decode attention HBM throughput (algorithmic bytes of all
 decode launches / their summed HIP-event durations); the masked-prefill
-TFLOP/s is reported beside it.  Prints one JSON line.
+TFLOP/s is reported beside it (roofline_prefill).
+
+The same line then carries, under "configs", the other workloads the metric
+names, each timed on its own after the previous one's buffers are freed:
+the OPT-1.3B-shaped prefill slice (b=8, H=32, d=64, L=2048), the OPT-1.3B-
+shaped compaction + 128 decode steps (24 layers, b=64), and the streaming
+workload (b=256, 1024 generated tokens, compaction after every <CR>) over
+its compressed cache.  cpu_baseline and cpu_baseline_prefill time the
+oracle's decode and prefill on a bounded sample, one thread per host core.
+Prints one JSON line.
 """
 from __future__ import annotations
 
@@ -46,7 +55,8 @@ def parse():
     ap.add_argument("--decode-steps", type=int, default=None)
     ap.add_argument("--launch-events", choices=["all", "none"], default="all")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="wall seconds of each CPU-baseline leg (decode, prefill)")
     ap.add_argument("--gen-tokens", type=int, default=None,
                     help="streaming workload: generated tokens per run (default: all)")
     ap.add_argument("--prefill-block", type=int, default=0,
@@ -55,6 +65,12 @@ def parse():
     ap.add_argument("--local-attention", action="store_true",
                     help="the local-attention comparator: decode over a ring of the W most "
                          "recent tokens, W = the rows the compressed cache holds at its largest")
+    ap.add_argument("--no-extra-configs", action="store_true",
+                    help="the headline workload only (by default the OPT-1.3B prefill, the "
+                         "OPT-1.3B compaction + decode and the streaming workload follow it)")
+    ap.add_argument("--stream-tokens", type=int, default=None,
+                    help="generated tokens of the streaming run among the extra configs "
+                         "(default: all 1024)")
     ap.add_argument("--span-sweep", action="store_true",
                     help="span lengths U(2,25) at each of --sweep-ratios instead of the "
                          "workload's own spans")
@@ -116,6 +132,16 @@ def kept_rows(spans, L):
     return L - closed - open_cl
 
 
+def decode_call_bytes(n_keep, t, H, d, elt=2):
+    """Algorithmic HBM bytes of one decode call (one layer) at generated step
+    t after a prompt whose compaction left n_keep[s] rows per sequence: the
+    n_keep + t cache rows held before the step's own row (key and value), q,
+    k_new and v_new read, o and the new key/value row written."""
+    n_keep = np.asarray(n_keep, dtype=np.int64)
+    b = len(n_keep)
+    return int((n_keep + t).sum()) * H * d * elt * 2 + 6 * b * H * d * elt
+
+
 # ---------------------------------------------------------------------------
 # HBM traffic from stored rocprof counter summaries
 # ---------------------------------------------------------------------------
@@ -156,86 +182,143 @@ def stored_mfma_busy(name, workload, kernel):
 
 
 # ---------------------------------------------------------------------------
-# CPU baseline: the oracle on a bounded sample
+# CPU baseline: the oracle on a bounded sample, on the host's cores
 # ---------------------------------------------------------------------------
 
+def host_info():
+    """CPU model, usable cores and host RAM of the machine the bench runs on."""
+    model, ram = None, None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        with open("/proc/meminfo") as f:
+            for line in f:
+                if line.startswith("MemTotal"):
+                    ram = round(int(line.split()[1]) / 2 ** 20, 1)
+                    break
+    except OSError:
+        pass
+    return {"cpu_model": model, "host_cores": len(os.sched_getaffinity(0)), "host_ram_gib": ram}
+
+
+def run_threads(jobs, seconds):
+    """Runs each job (a callable taking a deadline and returning the work it
+    finished) on a thread of its own until `seconds` of wall time have
+    passed; returns (total work, wall seconds).  NumPy releases the GIL in
+    the oracle's array operations, so the threads run on separate cores."""
+    import concurrent.futures as cf
+    t0 = time.perf_counter()
+    deadline = t0 + seconds
+    with cf.ThreadPoolExecutor(len(jobs)) as ex:
+        done = sum(ex.map(lambda j: j(deadline), jobs))
+    return done, time.perf_counter() - t0
+
+
 def cpu_baseline(w, spans_all, k_in, v_in, q_dec, k_dec, v_dec, seconds):
-    """The oracle's decode (rotary + attention over its own compacted cache)
-    on whole (layer, sequence) samples until about `seconds` of CPU time."""
+    """The oracle's decode (rotary of q and k + attention over its own
+    compacted cache) on one (layer, sequence) slice per host core, all 32
+    heads, step after step, for about `seconds` of wall time; bytes counted
+    as for the GPU figure (cache rows read + q, k, v in, o and the new row
+    out)."""
     from oracle import sckv_oracle as O
-    cores = len(os.sched_getaffinity(0))
+    n_thr = len(os.sched_getaffinity(0))
     L, H, d, M, b = w.seq_len, w.heads, w.d_head, w.layers, w.batch
-    T = L + w.decode_steps
+    steps = q_dec.shape[0]
+    T = L + steps
     f = lambda t: t.detach().to("cpu").double().numpy()
-    bytes_done, t_dec, samples, steps_done = 0, 0.0, 0, 0
-    for i in range(M * b):
-        if t_dec >= seconds:
-            break
+    jobs, done_steps = [], [0] * n_thr
+    t_prep = time.perf_counter()
+    for i in range(n_thr):
         m, s = i % M, (i * 7) % b
         types = O.token_types(spans_all[s], T)
         pos = O.tie_positions(types)
-        K = np.stack([O.rope_rotate_half(f(k_in[m, s, h]), pos[:L], w.rope_theta) for h in range(H)])
+        K = np.stack([O.rope_rotate_half(f(k_in[m, s, h]), pos[:L], w.rope_theta)
+                      for h in range(H)]) if w.rope_theta > 0 else f(k_in[m, s])
         Kc = np.zeros((H, T, d)); Vc = np.zeros((H, T, d))
         Kc[:, :L], Vc[:, :L] = K, f(v_in[m, s])
         tok = np.zeros(T, np.int64); tok[:L] = np.arange(L)
         pp = np.zeros(T, np.int64); pp[:L] = pos[:L]
-        Kc, Vc, tok, pp, n, _ = O.compact_cache(Kc, Vc, tok, pp, L, types, L)
+        Kc, Vc, _, _, n0, _ = O.compact_cache(Kc, Vc, tok, pp, L, types, L)
         qd, kd, vd = f(q_dec[:, m, s]), f(k_dec[:, m, s]), f(v_dec[:, m, s])
-        for st in range(w.decode_steps):
-            t = L + st
-            t0 = time.perf_counter()
-            qr = np.stack([O.rope_rotate_half(qd[st, h][None], [pos[t]], w.rope_theta)[0] for h in range(H)])
-            kr = np.stack([O.rope_rotate_half(kd[st, h][None], [pos[t]], w.rope_theta)[0] for h in range(H)])
-            O.decode_attention(qr, kr, vd[st], Kc, Vc, n, types[t] == O.CL)
-            t_dec += time.perf_counter() - t0
-            Kc[:, n], Vc[:, n] = kr, vd[st]
-            n += 1
-            bytes_done += n * H * d * 2 * 2 + 6 * H * d * 2
-            steps_done += 1
-        samples += 1
-    return {"value": round(bytes_done / t_dec / 1e9, 4), "unit": "GB/s", "cores": cores,
-            "kind": "oracle",
-            "sample": f"fp64 NumPy oracle decode (rotary + attention over its own compacted "
-                      f"cache), {samples} whole (layer, sequence) slices x {H} heads x "
-                      f"{w.decode_steps} generated tokens = {steps_done} sequence-steps, "
-                      f"{t_dec:.1f} s of CPU time; bytes counted as for the GPU figure"}
 
+        def job(deadline, i=i, Kc=Kc, Vc=Vc, n0=n0, qd=qd, kd=kd, vd=vd, pos=pos, types=types):
+            work, n, st = 0, n0, 0
+            while time.perf_counter() < deadline:
+                t = L + st
+                qr, kr = qd[st], kd[st]
+                if w.rope_theta > 0:
+                    qr = np.stack([O.rope_rotate_half(qd[st, h][None], [pos[t]], w.rope_theta)[0]
+                                   for h in range(H)])
+                    kr = np.stack([O.rope_rotate_half(kd[st, h][None], [pos[t]], w.rope_theta)[0]
+                                   for h in range(H)])
+                O.decode_attention(qr, kr, vd[st], Kc, Vc, n, types[t] == O.CL)
+                work += n * H * d * 2 * 2 + 6 * H * d * 2
+                done_steps[i] += 1
+                Kc[:, n], Vc[:, n] = kr, vd[st]
+                n, st = n + 1, st + 1
+                if st == steps:  # start the slice's generation over
+                    n, st = n0, 0
+            return work
+        jobs.append(job)
+    t_prep = time.perf_counter() - t_prep
+    done, wall = run_threads(jobs, seconds)
+    return {"value": round(done / wall / 1e9, 4), "unit": "GB/s", "cores": n_thr,
+            "kind": "oracle", **host_info(),
+            "sample": f"fp64 NumPy oracle decode (rotary of q and k + attention over its own "
+                      f"compacted cache), {n_thr} threads, each on one whole (layer, sequence) "
+                      f"slice x {H} heads generating its {steps} tokens in a loop; "
+                      f"{sum(done_steps)} sequence-steps in {wall:.1f} s of wall time "
+                      f"(compacted caches prepared beforehand in {t_prep:.1f} s, untimed); "
+                      f"bytes counted as for the GPU figure"}
 
 
 def cpu_baseline_prefill(w, spans_all, q_in, k_in, v_in, seconds):
-    """The oracle's masked prefill (explicit mask, dense fp64) on whole
-    (layer, sequence, head) slices until about `seconds` of CPU time;
-    algorithmic flops (4*d per visible pair) per second."""
+    """The oracle's masked prefill (rotary at tied positions, then dense
+    fp64 attention under the explicit L x L mask) on whole (layer, sequence,
+    head) slices, one thread per host core, for about `seconds` of wall
+    time; algorithmic flops (4*d per visible pair) per second.  The mask of
+    the sampled sequence is built once beforehand (untimed), as the GPU path
+    builds its plan once per prompt."""
     from oracle import sckv_oracle as O
-    cores = len(os.sched_getaffinity(0))
+    n_thr = len(os.sched_getaffinity(0))
     L, H, d, M, b = w.seq_len, w.heads, w.d_head, w.layers, w.batch
+    s = 1 % b
     f = lambda t: t.detach().to("cpu").double().numpy()
-    flops, t_pf, heads = 0, 0.0, 0
-    for i in range(M * b):
-        if t_pf >= seconds:
-            break
-        m, s = i % M, (i * 7) % b
-        types = O.token_types(spans_all[s], L)
-        pos = O.tie_positions(types)
-        mask = O.attention_mask(types)
-        nnz = int(mask.sum())
-        for h in range(H):
-            if t_pf >= seconds:
-                break
+    t_mask = time.perf_counter()
+    types = O.token_types(spans_all[s], L)
+    pos = O.tie_positions(types)
+    mask = O.attention_mask(types)
+    nnz = int(mask.sum())
+    t_mask = time.perf_counter() - t_mask
+    heads = [0] * n_thr
+
+    def job(deadline, i):
+        work, k = 0, 0
+        while time.perf_counter() < deadline:
+            m, h = (i + k * n_thr) % M, (i * 5 + k) % H
             Q, K, V = f(q_in[m, s, h]), f(k_in[m, s, h]), f(v_in[m, s, h])
-            t0 = time.perf_counter()
             if w.rope_theta > 0:
                 Q = O.rope_rotate_half(Q, pos, w.rope_theta)
                 K = O.rope_rotate_half(K, pos, w.rope_theta)
             O.masked_attention(Q[None], K[None], V[None], mask)
-            t_pf += time.perf_counter() - t0
-            flops += 4 * d * nnz
-            heads += 1
-    return {"value": round(flops / t_pf / 1e12, 6), "unit": "TFLOP/s", "cores": cores,
-            "kind": "oracle",
-            "sample": f"fp64 NumPy oracle prefill (explicit {L}x{L} mask, dense), {heads} "
-                      f"(layer, sequence, head) slices, {t_pf:.1f} s of CPU time; algorithmic "
-                      f"flops (4*d per visible pair) as for the GPU figure"}
+            work += 4 * d * nnz
+            heads[i] += 1
+            k += 1
+        return work
+    done, wall = run_threads([lambda dl, i=i: job(dl, i) for i in range(n_thr)], seconds)
+    return {"value": round(done / wall / 1e12, 6), "unit": "TFLOP/s", "cores": n_thr,
+            "kind": "oracle", **host_info(),
+            "sample": f"fp64 NumPy oracle prefill (rotary, explicit {L}x{L} mask, dense), "
+                      f"{n_thr} threads over whole (layer, sequence, head) slices of one "
+                      f"sequence, {sum(heads)} slices in {wall:.1f} s of wall time (the "
+                      f"sequence's mask built once beforehand in {t_mask:.1f} s, untimed); "
+                      f"algorithmic flops (4*d per visible pair) as for the GPU figure"}
 
 
 # ---------------------------------------------------------------------------
@@ -261,14 +344,18 @@ def live_rows_schedule(spans, prompt, gen):
     return out, peak
 
 
-def run_streaming(args, w):
+def streaming_run(w, gen, mode, warmup_tokens):
+    """One streaming generation of `gen` tokens after the prompt, over the
+    compressed cache (spans freed after every <CR>) or an uncompressed one
+    (no spans); the cache is sized to the schedule's peak row count.
+    Returns figures for the timed run, which follows an untimed warm-up of
+    `warmup_tokens` tokens over the same cache."""
     import torch
 
     from paper_2310_08152_amd import path as P
     from paper_2310_08152_amd import workload as W
 
     dev = "cuda:0"
-    gen = w.gen_tokens if args.gen_tokens is None else args.gen_tokens
     M, b, H, d, L = w.layers, w.batch, w.heads, w.d_head, w.seq_len
     T = L + gen
     dt = W.torch_dtype(w.dtype)
@@ -277,54 +364,65 @@ def run_streaming(args, w):
     kp = W.randn((POOL, M, b, H, d), seed=w.seed * 100000 + 2, dtype=w.dtype, device=dev)
     vp = W.randn((POOL, M, b, H, d), seed=w.seed * 100000 + 3, dtype=w.dtype, device=dev)
     od = torch.empty(b, H, d, dtype=dt, device=dev)
+    spans = [[(c, r) for c, r in s if c < T] for s in W.workload_spans(w)] \
+        if mode == "compressed" else [[] for _ in range(b)]
+    sched, peak = live_rows_schedule(spans[0], L, gen)
+    L_cap = peak
+    cr_steps = {r for c, r in spans[0] if L <= r < T}
+    meta = P.SpanMeta(spans, T, dev)
+    cache = P.KVCache(M, b, H, L_cap, d, dt, dev)
+    for m in range(M):
+        for kv in range(2):
+            cache.kv[m, kv, :, :, :L].copy_(W.randn((b, H, L, d), seed=w.seed * 1000 + m * 2 + kv,
+                                                    dtype=w.dtype, device=dev))
+    ws = P.Workspace(b, H, 1, L_cap, d, dev)
+
+    def loop(n_tok):
+        cache.start_prompt(L, meta)
+        for t in range(n_tok):
+            i = t % POOL
+            for m in range(M):
+                P.decode_layer(qp[i, m], kp[i, m], vp[i, m], cache, m, meta, ws, od,
+                               theta=w.rope_theta)
+            cache.commit(meta)
+            if L + t in cr_steps:
+                cache.compact(meta)
+
+    if warmup_tokens:
+        loop(min(warmup_tokens, gen))
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    loop(gen)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    if int(cache.status):
+        raise RuntimeError(f"device status {int(cache.status)}")
+    assert cache.kv_len.tolist() == [sched[-1]] * b, (cache.kv_len.tolist()[:4], sched[-1])
+    row_b = d * 2
+    # rows read by the decode launches: every step attends to the rows held
+    # before its own (sched[t-1], the prompt's L at the first step)
+    rows_read = sum([L] + sched[:-1])
+    attn_bytes = rows_read * b * H * M * row_b * 2 + gen * M * 6 * b * H * d * 2
+    gbs = attn_bytes / (ms * 1e-3) / 1e9
+    return {"tokens_per_s": round(b * gen / (ms * 1e-3), 1), "ms": round(ms, 2),
+            "generated": gen, "peak_rows": peak, "final_rows": sched[-1],
+            "span_closes": len([r for r in cr_steps if r < L + gen]),
+            "cache_bytes": int(cache.kv.numel() * cache.kv.element_size()),
+            "attn_gbs": round(gbs, 1), "attn_frac_of_hbm": round(gbs / HBM_PEAK_GBS, 4),
+            "attn_gbs_note": "decode bytes (cache rows read + q/k/v in, o and the new row out) "
+                             "over the whole loop's time, commits and compactions included"}
+
+
+def run_streaming(args, w):
+    import torch
+
+    gen = w.gen_tokens if args.gen_tokens is None else args.gen_tokens
+    M, b, H, d, L = w.layers, w.batch, w.heads, w.d_head, w.seq_len
     results = {}
     for mode in ("compressed", "uncompressed"):
-        spans = [[(c, r) for c, r in s if c < T] for s in W.workload_spans(w)] \
-            if mode == "compressed" else [[] for _ in range(b)]
-        sched, peak = live_rows_schedule(spans[0], L, gen)
-        L_cap = peak
-        cr_steps = {r for c, r in spans[0] if L <= r < T}
-        meta = P.SpanMeta(spans, T, dev)
-        cache = P.KVCache(M, b, H, L_cap, d, dt, dev)
-        for m in range(M):
-            for kv in range(2):
-                cache.kv[m, kv, :, :, :L].copy_(W.randn((b, H, L, d), seed=w.seed * 1000 + m * 2 + kv,
-                                                        dtype=w.dtype, device=dev))
-        ws = P.Workspace(b, H, 1, L_cap, d, dev)
-
-        def loop():
-            cache.start_prompt(L, meta)
-            for t in range(gen):
-                i = t % POOL
-                for m in range(M):
-                    P.decode_layer(qp[i, m], kp[i, m], vp[i, m], cache, m, meta, ws, od,
-                                   theta=w.rope_theta)
-                cache.commit(meta)
-                if L + t in cr_steps:
-                    cache.compact(meta)
-
-        if args.warmup:
-            loop()
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        loop()
-        e1.record()
-        torch.cuda.synchronize()
-        ms = e0.elapsed_time(e1)
-        if int(cache.status):
-            raise RuntimeError(f"device status {int(cache.status)}")
-        assert cache.kv_len.tolist() == [sched[-1]] * b, (cache.kv_len.tolist()[:4], sched[-1])
-        row_b = d * 2
-        rows_read = sum(sched[t] for t in range(gen))  # rows attended per (seq, head, layer)
-        results[mode] = {
-            "tokens_per_s": round(b * gen / (ms * 1e-3), 1),
-            "ms": round(ms, 2),
-            "peak_rows": peak, "final_rows": sched[-1],
-            "cache_bytes": int(cache.kv.numel() * cache.kv.element_size()),
-            "attn_gbs": round(rows_read * b * H * M * row_b * 2 / (ms * 1e-3) / 1e9, 1),
-        }
-        del cache, meta, ws
+        results[mode] = streaming_run(w, gen, mode, gen if args.warmup else 0)
         torch.cuda.empty_cache()
     c, u = results["compressed"], results["uncompressed"]
     out = {
@@ -341,6 +439,62 @@ def run_streaming(args, w):
         "kv_bytes_saved": u["cache_bytes"] - c["cache_bytes"],
     }
     print(json.dumps(out), flush=True)
+
+
+def extra_configs(args):
+    """The other workloads the metric names, each timed on its own after the
+    headline workload's buffers are freed: the OPT-1.3B-shaped prefill slice,
+    the OPT-1.3B-shaped compaction + decode, and the streaming workload over
+    its compressed cache."""
+    import copy
+
+    import torch
+
+    from paper_2310_08152_amd import workload as W
+
+    out = {}
+    a = copy.copy(args)
+    a.no_cpu_baseline = True
+    a.decode_steps = None
+    w2 = W.get_workload("opt1.3b-prefill")
+    r = measure(a, w2)
+    pf = r["roofline"]
+    out[w2.name] = {
+        "workload": f"{w2.name}: masked prefill, {w2.layers} layer, b={w2.batch}, H={w2.heads}, "
+                    f"d={w2.d_head}, L={w2.seq_len}, {r['config']['evicted']:.0%} freed",
+        "prefill_tflops_algorithmic": pf["achieved"], "frac_algorithmic": pf["frac"],
+        "prefill_tflops_executed": pf["executed_tflops"],
+        "frac_executed": round(pf["executed_tflops"] / BF16_PEAK_TFLOPS, 4),
+        "executed_over_algorithmic": pf["executed_over_algorithmic"],
+        "avg_launch_us": pf["avg_launch_us"], "plan_us": pf["plan_us"],
+        "timed_steps": a.steps}
+    torch.cuda.empty_cache()
+    w3 = W.get_workload("opt1.3b-decode")
+    a.steps, a.warmup = min(args.steps, 3), 1
+    r = measure(a, w3)
+    dec, pf = r["roofline"], r["roofline_prefill"]
+    out[w3.name] = {
+        "workload": f"{w3.name}: {w3.layers} layers, b={w3.batch}, H={w3.heads}, d={w3.d_head}, "
+                    f"L={w3.seq_len}, {r['config']['evicted']:.0%} freed, "
+                    f"{w3.decode_steps} decode steps",
+        "decode_gbs": dec["achieved"], "decode_frac": dec["frac"],
+        "decode_avg_launch_us": dec["avg_launch_us"], "decode_bytes_per_launch":
+            dec["bytes_per_launch"],
+        "compaction_gbs": r["compaction_gbs"],
+        "compaction_frac": round(r["compaction_gbs"] / HBM_PEAK_GBS, 4),
+        "compaction_bytes": r["compaction_bytes"], "compaction_ms": r["phases_ms"]["compaction"],
+        "prefill_tflops_algorithmic": pf["achieved"], "prefill_frac_algorithmic": pf["frac"],
+        "prefill_tflops_executed": pf["executed_tflops"],
+        "decode_tokens_per_s": r["decode_tokens_per_s"], "timed_steps": a.steps}
+    torch.cuda.empty_cache()
+    w5 = W.get_workload("3b-rope-stream")
+    gen = w5.gen_tokens if args.stream_tokens is None else args.stream_tokens
+    c = streaming_run(w5, gen, "compressed", 16)
+    out[w5.name] = {"workload": f"{w5.name}: {w5.layers} layers, b={w5.batch}, H={w5.heads}, "
+                                f"d={w5.d_head}, prompt {w5.seq_len}, {gen} generated tokens, "
+                                f"compressed cache, compaction after every <CR>", **c}
+    torch.cuda.empty_cache()
+    return out
 
 
 # ---------------------------------------------------------------------------
@@ -367,7 +521,11 @@ def main():
         return run_span_sweep(args, w)
     if args.local_attention:
         return run_local_attention(args, w)
-    print(json.dumps(measure(args, w)), flush=True)
+    out = measure(args, w)
+    if args.workload == "3b-rope" and args.prefill_block == 0 and not args.no_extra_configs:
+        torch.cuda.empty_cache()
+        out["configs"] = extra_configs(args)
+    print(json.dumps(out), flush=True)
 
 
 def measure(args, w):
@@ -487,9 +645,7 @@ def measure(args, w):
     # ---- accounting ----
     n_keep = np.array([kept_rows(s, L) for s in spans_all], dtype=np.int64)
     assert np.array_equal(cache.kv_len.cpu().numpy(), n_keep + steps), "unexpected kv_len"
-    row_bytes = d * 2 * 2                    # one K row + one V row (bf16)
-    io_bytes = 6 * b * H * d * 2             # q, k_new, v_new read; o, new K/V row written
-    dec_bytes = [int((n_keep + t + 1).sum()) * H * row_bytes + io_bytes for t in range(steps)]
+    dec_bytes = [decode_call_bytes(n_keep, t, H, d) for t in range(steps)]
     dec_bytes_step = M * sum(dec_bytes)
     pf_alg, pf_exe = prefill_work(spans_all, L, H, d)
     comp_bytes = 0
@@ -608,6 +764,9 @@ def measure(args, w):
     elif not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, spans_all, k_in, v_in, q_dec, k_dec, v_dec,
                                            args.cpu_seconds)
+        # the oracle's prefill beside roofline_prefill
+        out["cpu_baseline_prefill"] = cpu_baseline_prefill(w, spans_all, q_in, k_in, v_in,
+                                                           args.cpu_seconds)
     elt = 2 if w.dtype == "bf16" else 4
     live = int(n_keep.max()) + steps  # rows held by the longest sequence at the last step
     if pb > 0:

@@ -44,6 +44,25 @@ def test_kept_rows_equal_oracle_keep_flags(L, ratio, seed):
         assert bench.kept_rows(sub, P) == int(O.keep_rows(types[:P], P).sum())
 
 
+@pytest.mark.parametrize("L,ratio,seed", [(96, 0.4, 8), (300, 0.75, 9)])
+def test_decode_bytes_follow_the_oracles_cache(L, ratio, seed):
+    """The decode byte count of a step is the rows the oracle's compacted
+    cache holds before that step (read as key and value) plus q, k, v in and
+    o and the new row out, nothing for the step's own row twice."""
+    H, d, steps = 2, 16, 5
+    spans_all = [random_spans(L, ratio, seed + s) for s in range(3)]
+    n_keep = [bench.kept_rows(sp, L) for sp in spans_all]
+    for t in range(steps):
+        rows = 0
+        for sp in spans_all:
+            types = O.token_types(sp, L + steps)
+            cache = O.compact_cache(np.zeros((1, L + steps, 1)), np.zeros((1, L + steps, 1)),
+                                    np.arange(L + steps), np.arange(L + steps), L, types, L)
+            rows += cache[4] + t  # no spans after the prompt: every step appends
+        want = rows * H * d * 2 * 2 + 6 * len(spans_all) * H * d * 2
+        assert bench.decode_call_bytes(n_keep, t, H, d) == want
+
+
 def test_multi_gpu_request_exits_with_message():
     r = subprocess.run([sys.executable, "bench.py", "--gpus", "2"], capture_output=True,
                        text=True, timeout=120)
