@@ -49,6 +49,10 @@ constexpr int PF_BK = 64;
 // a block's list has room for at least two tiles (its first two are loaded early)
 static_assert(PF_BQ >= 2 * PF_BK, "list of at least two tiles");
 constexpr int PF_THREADS = 64 * PF_WAVES;
+// (sequence, head) slices whose query blocks are ordered together,
+// heaviest first (a dispatch simulation over the two prompt shapes puts
+// groups of 8 within 3-6% of an ideal balance, against 9-18% for one slice)
+constexpr int PF_GROUP = 8;
 constexpr uint32_t PF_NONE = 0x00ffffffu;  // list entry of a padding column
 constexpr float PF_LOG2E = 1.4426950408889634f;
 // The running maximum of a query row is only moved (and the accumulators
@@ -239,14 +243,23 @@ __device__ __forceinline__ void prefill_attn_body(
   __shared__ int32_t row_ring[PF_ER][PF_BK];  // bare row index per entry
   __shared__ TileInfo info_ring[PF_ER];
 
-  // XCD-aware work order: consecutive work items (same (sequence, head),
-  // heaviest query block first) land on the same XCD and share its L2.
+  // Work order.  Workgroup x is dispatched to XCD x mod 8, and each XCD takes
+  // a contiguous range of work items in dispatch order, so the items of a
+  // group of PF_GROUP consecutive (sequence, head) slices share that XCD's
+  // L2.  Inside a group the items go heaviest first: every head's last
+  // query block (the most visible keys), then every head's block before it,
+  // and so on, so that the light blocks fill the end of the launch instead
+  // of one slice's heavy block running alone there.
   const int x = blockIdx.x;
   const int xcd = x & 7, idx = x >> 3;
   const int qn = n_work >> 3, rem = n_work & 7;
   const int work = xcd * qn + min(xcd, rem) + idx;
-  const int bh = work / n_qt;
-  const int qt = n_qt - 1 - (work % n_qt);
+  const int nbh = n_work / n_qt;
+  const int grp = work / (PF_GROUP * n_qt);
+  const int gsz = min(PF_GROUP, nbh - grp * PF_GROUP);
+  const int in_grp = work - grp * PF_GROUP * n_qt;
+  const int bh = grp * PF_GROUP + in_grp % gsz;
+  const int qt = n_qt - 1 - in_grp / gsz;
   const int s = bh / H;
   // query rows are local (0 .. L-1); their tokens start at tok0 (cached) or 0
   const int tok0 = CACHED ? cc.tok0 : 0;
