@@ -170,9 +170,15 @@ template <int D> struct PfCfg<uint16_t, D> {
   static constexpr int DP = (D + 31) / 32 * 32;     // value columns padded to whole 32-row MFMA blocks
   static constexpr int KP = D + 8;                  // K tile: [64][KP] bf16 (one 16-byte pad slot)
   // V tile: [64][VP] bf16, row-major like K; the PV operand is read with the
-  // transposing LDS read.  A 192-byte pitch puts the four rows one
-  // transposing read touches in disjoint groups of 16 banks.
-  static constexpr int VP = 96;
+  // transposing LDS read.  With a ones row (D = 80) the pitch is 192 bytes,
+  // which puts the four rows one transposing read touches in disjoint groups
+  // of 16 banks.  At D = 64 the rows are unpadded (128 bytes) and the
+  // 16-byte pieces of a row are swizzled instead: logical piece p of row r
+  // sits in slot p ^ (4 * bit 1 of r), which spreads the rows of one
+  // transposing read over the banks the same way in two thirds of the space.
+  static constexpr bool VSWZ = (D == 64);
+  static constexpr int VP = VSWZ ? D : 96;
+  static constexpr int NB = D == 64 ? 1 : 2;        // 32-key blocks per softmax step
   static_assert(DP <= VP, "value tile pitch");
   static constexpr int E = 8;                       // elements per 16-byte slot
   static constexpr int KSTEPS = D / 16;
@@ -180,6 +186,8 @@ template <int D> struct PfCfg<uint16_t, D> {
 
 template <int D> struct PfCfg<float, D> {
   static constexpr int NBUF = 1;
+  static constexpr bool VSWZ = false;
+  static constexpr int NB = 2;
   static constexpr int DP = (D + 31) / 32 * 32;
   static constexpr int KP = D + 4;                  // K tile: [64][KP] f32
   static constexpr int VP = DP + 8;                 // V tile: [64][VP] f32 (row-major)
@@ -443,7 +451,11 @@ __device__ __forceinline__ void prefill_attn_body(
     const int sl = (rnd * PF_WAVES + wave) * 64 + lane;
     const int sg = sl % TL::VSLOT;
     v_row[rnd] = min(sl / TL::VSLOT, PF_BK - 1);
-    v_off[rnd] = sg < TL::PPR ? sg * 16 : -1;
+    int vpiece = sg;  // the logical piece slot sg holds
+    if constexpr (BF) {
+      if constexpr (C::VSWZ) vpiece = sg ^ (((v_row[rnd] >> 1) & 1) << 2);
+    }
+    v_off[rnd] = sg < TL::PPR ? vpiece * 16 : -1;
   }
   auto dma_rows = [&](int kt, char* kdst, char* vdst) {
     const int32_t* rows = row_ring[kt % PF_ER];
@@ -468,118 +480,144 @@ __device__ __forceinline__ void prefill_attn_body(
     }
   };
 
+  // Transposing-read addresses of the V^T operand, per 32-column block db
+  // of the value tile: within each group of 16 lanes, lane j points at
+  // V[kbase + j/4][dbase + 4*(j%4)]; the read hands lane i the four keys
+  // kbase..kbase+3 of column dbase + i.  Offsets in elements from the tile
+  // start; a step t of 16 keys adds (16 t) rows, its upper 8 keys 8 rows.
+  int v_lane_off[NDB];
+  {
+    const int G = lane >> 4, j16 = lane & 15;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+      const int col = 32 * db + 16 * (G & 1) + 4 * (j16 & 3);
+      const int row = 4 * g + (j16 >> 2);  // bit 1 of the row is bit 1 of j16 >> 2
+      if constexpr (BF && C::VSWZ)
+        v_lane_off[db] = row * C::VP + (((col >> 3) ^ (((row >> 1) & 1) << 2)) << 3) + (col & 7);
+      else
+        v_lane_off[db] = row * C::VP + col;
+    }
+  }
+
   // summary of the tile being computed, read from the ring one step early
   // so that the step starts with its key reads
   TileInfo tcur;
+  // A 64-key tile is weighed in softmax steps of NB 32-key blocks: scores
+  // of the step, its online softmax, its share of the value product.  At
+  // D = 64 a step is one block (32 keys), so only half a tile's scores and
+  // probabilities are live at a time and four waves fit per SIMD; at D = 80
+  // a step is the whole tile (measured faster there, at three waves either
+  // way).
+  constexpr int NB = C::NB;
   auto compute = [&](int kt, const char* kcur, const char* vcur) {
     const TileInfo ti = tcur;
     const uint32_t* tent = ent_ring[kt % PF_ER];
     if (wave_live && ti.jmin <= Iw + 31) {
       const bool full = ti.nvalid == PF_BK && ti.jmax <= Iw && ti.vrmin >= Iw + 31 - I;
-      // ---- S^T = K Q^T for the two 32-key blocks, key step outer so that
-      // consecutive matrix instructions write different accumulators ----
-      f32x16 sacc[2];
 #pragma unroll
-      for (int kb2 = 0; kb2 < 2; ++kb2)
+      for (int st = 0; st < 2 / NB; ++st) {
+        // ---- S^T = K Q^T for the step's key blocks, key step outer so that
+        // consecutive matrix instructions write different accumulators ----
+        f32x16 sacc[NB];
 #pragma unroll
-        for (int i = 0; i < 16; ++i) sacc[kb2][i] = 0.f;
+        for (int kb = 0; kb < NB; ++kb)
 #pragma unroll
-      for (int kk = 0; kk < C::KSTEPS; ++kk) {
+          for (int i = 0; i < 16; ++i) sacc[kb][i] = 0.f;
 #pragma unroll
-        for (int kb2 = 0; kb2 < 2; ++kb2) {
-          if constexpr (BF) {
-            const char* krow = kcur + ((kb2 * 32 + l32) * C::KP + g * 8 + kk * 16) * 2;
-            const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(krow));
-            sacc[kb2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[kk], sacc[kb2], 0, 0, 0);
-          } else {
-            const float* krow = reinterpret_cast<const float*>(kcur) + (kb2 * 32 + l32) * C::KP + g;
-            sacc[kb2] = __builtin_amdgcn_mfma_f32_32x32x2f32(krow[2 * kk], qreg[kk], sacc[kb2], 0, 0, 0);
+        for (int kk = 0; kk < C::KSTEPS; ++kk) {
+#pragma unroll
+          for (int kb = 0; kb < NB; ++kb) {
+            const int kb2 = st * NB + kb;
+            if constexpr (BF) {
+              const char* krow = kcur + ((kb2 * 32 + l32) * C::KP + g * 8 + kk * 16) * 2;
+              const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(krow));
+              sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[kk], sacc[kb], 0, 0, 0);
+            } else {
+              const float* krow = reinterpret_cast<const float*>(kcur) + (kb2 * 32 + l32) * C::KP + g;
+              sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x2f32(krow[2 * kk], qreg[kk], sacc[kb], 0, 0, 0);
+            }
           }
         }
-      }
-      // ---- element mask on tiles not entirely visible to this wave ----
-      if (!full) {
-        const int ir = qtok - I;
+        // ---- element mask on tiles not entirely visible to this wave ----
+        if (!full) {
+          const int ir = qtok - I;
 #pragma unroll
-        for (int kb2 = 0; kb2 < 2; ++kb2)
-#pragma unroll
-          for (int vv = 0; vv < 16; ++vv) {
-            const int key = kb2 * 32 + 8 * (vv >> 2) + 4 * g + (vv & 3);
-            const uint32_t e = tent[key];
-            const int j = (int)(e & 0x00ffffffu);
-            const int vr = (int)(e >> 24);
-            const bool vis = (j <= qtok) & (ir <= vr);
-            sacc[kb2][vv] = vis ? sacc[kb2][vv] : -INFINITY;
-          }
-      }
-      // ---- online softmax (log2 units), lazy rescaling ----
-      float mx = -INFINITY;
-#pragma unroll
-      for (int kb2 = 0; kb2 < 2; ++kb2)
-#pragma unroll
-        for (int vv = 0; vv < 16; ++vv) mx = fmaxf(mx, sacc[kb2][vv]);
-      mx = max_across_halves(mx) * c2;
-      const bool grow = mx > m_run + PF_RESCALE;
-      if (__ballot(grow) != 0) {
-        const float alpha = grow ? fast_exp2(m_run - mx) : 1.f;  // m_run == -inf gives 0
-        if (grow) m_run = mx;
-        l_run *= alpha;
-#pragma unroll
-        for (int db = 0; db < NDB; ++db)
-#pragma unroll
-          for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
-      }
-      const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
-      float rs = 0.f;
-#pragma unroll
-      for (int kb2 = 0; kb2 < 2; ++kb2)
-#pragma unroll
-        for (int vv = 0; vv < 16; ++vv) {
-          const float p = fast_exp2(fmaf(sacc[kb2][vv], c2, -m_use));
-          sacc[kb2][vv] = p;
-          if constexpr (!ONES_SUM) rs += p;
-        }
-      if constexpr (!ONES_SUM) l_run += rs;
-      // ---- O^T += V^T P^T ----
-      if constexpr (BF) {
-        bf16x8 pb[4];
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          u32x4 w;
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            w[i] = pack_bf16x2(sacc[t >> 1][8 * (t & 1) + 2 * i], sacc[t >> 1][8 * (t & 1) + 2 * i + 1]);
-          pb[t] = __builtin_bit_cast(bf16x8, w);
-        }
-        // A operand V^T[d][keys]: within each group of 16 lanes, lane j points
-        // at V[kbase + j/4][dbase + 4*(j%4)]; the transposing read hands lane
-        // i the four keys kbase..kbase+3 of column dbase + i.
-        const uint16_t* vs = reinterpret_cast<const uint16_t*>(vcur);
-        const int G = lane >> 4, j16 = lane & 15;
-        const uint16_t* vsrc = vs + (4 * g + (j16 >> 2)) * C::VP + 16 * (G & 1) + 4 * (j16 & 3);
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-#pragma unroll
-          for (int db = 0; db < NDB; ++db) {
-            const s16x4 lo = lds_read_tr16(vsrc + (16 * t) * C::VP + 32 * db);
-            const s16x4 hi = lds_read_tr16(vsrc + (16 * t + 8) * C::VP + 32 * db);
-            const s16x8 w = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-            oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, w), pb[t],
-                                                               oacc[db], 0, 0, 0);
-          }
-        }
-      } else {
-        const float* vs = reinterpret_cast<const float*>(vcur);
-#pragma unroll
-        for (int db = 0; db < NDB; ++db)
-#pragma unroll
-          for (int kb2 = 0; kb2 < 2; ++kb2)
+          for (int kb = 0; kb < NB; ++kb)
 #pragma unroll
             for (int vv = 0; vv < 16; ++vv) {
-              const int key = kb2 * 32 + 8 * (vv >> 2) + 4 * g + (vv & 3);
-              oacc[db] = __builtin_amdgcn_mfma_f32_32x32x2f32(vs[key * C::VP + db * 32 + l32],
-                                                              sacc[kb2][vv], oacc[db], 0, 0, 0);
+              const int key = (st * NB + kb) * 32 + 8 * (vv >> 2) + 4 * g + (vv & 3);
+              const uint32_t e = tent[key];
+              const int j = (int)(e & 0x00ffffffu);
+              const int vr = (int)(e >> 24);
+              const bool vis = (j <= qtok) & (ir <= vr);
+              sacc[kb][vv] = vis ? sacc[kb][vv] : -INFINITY;
             }
+        }
+        // ---- online softmax (log2 units), lazy rescaling ----
+        float mx = -INFINITY;
+#pragma unroll
+        for (int kb = 0; kb < NB; ++kb)
+#pragma unroll
+          for (int vv = 0; vv < 16; ++vv) mx = fmaxf(mx, sacc[kb][vv]);
+        mx = max_across_halves(mx) * c2;
+        const bool grow = mx > m_run + PF_RESCALE;
+        if (__ballot(grow) != 0) {
+          const float alpha = grow ? fast_exp2(m_run - mx) : 1.f;  // m_run == -inf gives 0
+          if (grow) m_run = mx;
+          l_run *= alpha;
+#pragma unroll
+          for (int db = 0; db < NDB; ++db)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
+        }
+        const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
+        float rs = 0.f;
+#pragma unroll
+        for (int kb = 0; kb < NB; ++kb)
+#pragma unroll
+          for (int vv = 0; vv < 16; ++vv) {
+            const float p = fast_exp2(fmaf(sacc[kb][vv], c2, -m_use));
+            sacc[kb][vv] = p;
+            if constexpr (!ONES_SUM) rs += p;
+          }
+        if constexpr (!ONES_SUM) l_run += rs;
+        // ---- O^T += V^T P^T over the step's keys, 16 at a time ----
+        if constexpr (BF) {
+          bf16x8 pb[2 * NB];
+#pragma unroll
+          for (int tt = 0; tt < 2 * NB; ++tt) {
+            u32x4 w;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              w[i] = pack_bf16x2(sacc[tt >> 1][8 * (tt & 1) + 2 * i], sacc[tt >> 1][8 * (tt & 1) + 2 * i + 1]);
+            pb[tt] = __builtin_bit_cast(bf16x8, w);
+          }
+          const uint16_t* vs = reinterpret_cast<const uint16_t*>(vcur);
+#pragma unroll
+          for (int tt = 0; tt < 2 * NB; ++tt) {
+            const int t = 2 * NB * st + tt;
+#pragma unroll
+            for (int db = 0; db < NDB; ++db) {
+              const s16x4 lo = lds_read_tr16(vs + v_lane_off[db] + (16 * t) * C::VP);
+              const s16x4 hi = lds_read_tr16(vs + v_lane_off[db] + (16 * t + 8) * C::VP);
+              const s16x8 vw = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+              oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vw),
+                                                                 pb[tt], oacc[db], 0, 0, 0);
+            }
+          }
+        } else {
+          const float* vs = reinterpret_cast<const float*>(vcur);
+#pragma unroll
+          for (int db = 0; db < NDB; ++db)
+#pragma unroll
+            for (int kb = 0; kb < NB; ++kb)
+#pragma unroll
+              for (int vv = 0; vv < 16; ++vv) {
+                const int key = (st * NB + kb) * 32 + 8 * (vv >> 2) + 4 * g + (vv & 3);
+                oacc[db] = __builtin_amdgcn_mfma_f32_32x32x2f32(vs[key * C::VP + db * 32 + l32],
+                                                                sacc[kb][vv], oacc[db], 0, 0, 0);
+              }
+        }
       }
     }
   };
@@ -639,30 +677,39 @@ __device__ __forceinline__ void prefill_attn_body(
   }
   if (qrow >= L || is_cl) return;
   const float inv = 1.f / l_tot;
+  // The output row's address is recomputed here from an opaque copy of the
+  // lane index rather than kept from the start of the kernel: holding it
+  // (and the lane's column offset) across the tile loop costs registers the
+  // loop needs.
+  int lane_e = threadIdx.x & 63;
+  asm volatile("" : "+v"(lane_e));
+  T* const orow_e = o + (int64_t)bh * os + (int64_t)(Iw_loc + (lane_e & 31)) * D + 4 * (lane_e >> 5);
 #pragma unroll
   for (int db = 0; db < NDB; ++db)
 #pragma unroll
     for (int jj = 0; jj < 4; ++jj) {
-      const int d0 = db * 32 + 8 * jj + 4 * g;
-      if (d0 >= D) continue;
+      const int d0 = db * 32 + 8 * jj;
+      if (d0 >= D) continue;  // D and d0 are multiples of 8
       if constexpr (BF) {
         u32x2 w;
         w[0] = pack_bf16x2(oacc[db][4 * jj] * inv, oacc[db][4 * jj + 1] * inv);
         w[1] = pack_bf16x2(oacc[db][4 * jj + 2] * inv, oacc[db][4 * jj + 3] * inv);
-        *reinterpret_cast<u32x2*>(orow + d0) = w;
+        *reinterpret_cast<u32x2*>(orow_e + d0) = w;
       } else {
         u32x4 w;
 #pragma unroll
         for (int i = 0; i < 4; ++i) w[i] = __float_as_uint(oacc[db][4 * jj + i] * inv);
-        st16(orow + d0, w);
+        st16(orow_e + d0, w);
       }
     }
 }
 
-// bf16 runs at three waves per SIMD (at most 168 registers), measured faster
-// than two and than four; the fp32 variant (small parity cases) is not capped.
+// bf16 runs at four waves per SIMD at D = 64 (at most 128 registers; 36.9 KB
+// of LDS per workgroup, so four workgroups share a CU) and at three at D = 80
+// (at most 168 registers; 49 KB of LDS), each measured faster than one wave
+// fewer; the fp32 variant (small parity cases) is not capped.
 template <int D, bool CACHED>
-__global__ __launch_bounds__(PF_THREADS) __attribute__((amdgpu_waves_per_eu(3))) void prefill_attn_kernel_bf16(
+__global__ __launch_bounds__(PF_THREADS) __attribute__((amdgpu_waves_per_eu(D == 64 ? 4 : 3))) void prefill_attn_kernel_bf16(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     uint16_t* __restrict__ o, int32_t H, int32_t L, int64_t qs, int64_t kvs, int64_t os, float c2,
     const int32_t* __restrict__ vu, int32_t L_meta, const uint32_t* __restrict__ list,
