@@ -444,7 +444,9 @@ __device__ __forceinline__ void prefill_attn_body(
     const int sl = (rnd * PF_WAVES + wave) * 64 + lane;
     const int sg = sl % TL::KSLOT;
     k_row[rnd] = min(sl / TL::KSLOT, PF_BK - 1);
-    k_off[rnd] = sg < TL::PPR ? sg * 16 : -1;
+    // a key row's pad slot is never read, so it is copied too (whatever the
+    // 16 bytes after the row hold): no lane of a copy is masked off
+    k_off[rnd] = sg * 16;
   }
 #pragma unroll
   for (int rnd = 0; rnd < VRND; ++rnd) {
@@ -455,6 +457,8 @@ __device__ __forceinline__ void prefill_attn_body(
     if constexpr (BF) {
       if constexpr (C::VSWZ) vpiece = sg ^ (((v_row[rnd] >> 1) & 1) << 2);
     }
+    // the value tile's pad slots hold the ones row and zeros (D = 80) and
+    // must not be overwritten; without them (D = 64) every slot is data
     v_off[rnd] = sg < TL::PPR ? vpiece * 16 : -1;
   }
   auto dma_rows = [&](int kt, char* kdst, char* vdst) {
@@ -467,14 +471,14 @@ __device__ __forceinline__ void prefill_attn_body(
 #pragma unroll
     for (int rnd = 0; rnd < KRND; ++rnd) {
       const int blk = rnd * PF_WAVES + wave_s;
-      if (blk < TL::KSLOT && k_off[rnd] >= 0)
+      if (blk < TL::KSLOT)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(krs, (lds_ptr_t)(kdst + blk * 1024), 16,
                                                  kj[rnd] * ROWB + k_off[rnd], 0, 0, 0);
     }
 #pragma unroll
     for (int rnd = 0; rnd < VRND; ++rnd) {
       const int blk = rnd * PF_WAVES + wave_s;
-      if (blk < TL::VSLOT && v_off[rnd] >= 0)
+      if (blk < TL::VSLOT && (TL::VSLOT == TL::PPR || v_off[rnd] >= 0))
         __builtin_amdgcn_raw_ptr_buffer_load_lds(vrs, (lds_ptr_t)(vdst + blk * 1024), 16,
                                                  vj[rnd] * ROWB + v_off[rnd], 0, 0, 0);
     }
