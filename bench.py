@@ -467,6 +467,10 @@ def extra_configs(args):
         "frac_executed": round(pf["executed_tflops"] / BF16_PEAK_TFLOPS, 4),
         "executed_over_algorithmic": pf["executed_over_algorithmic"],
         "avg_launch_us": pf["avg_launch_us"], "plan_us": pf["plan_us"],
+        "traffic": stored_traffic("traffic_prefill_opt1.3b-prefill.json", f"{w2.name}/steps0"),
+        "traffic_unit": "HBM bytes per call (rocprofv3 FETCH_SIZE + WRITE_SIZE, calibrated)",
+        "mfma_busy": stored_mfma_busy("mfma_opt1.3b-prefill.json", f"{w2.name}/steps0",
+                                      "prefill_attn_kernel"),
         "timed_steps": a.steps}
     torch.cuda.empty_cache()
     w3 = W.get_workload("opt1.3b-decode")
@@ -483,6 +487,10 @@ def extra_configs(args):
         "compaction_gbs": r["compaction_gbs"],
         "compaction_frac": round(r["compaction_gbs"] / HBM_PEAK_GBS, 4),
         "compaction_bytes": r["compaction_bytes"], "compaction_ms": r["phases_ms"]["compaction"],
+        "decode_traffic": stored_traffic("traffic_decode_opt1.3b-decode.json",
+                                         f"{w3.name}/steps{w3.decode_steps}"),
+        "compaction_traffic": stored_traffic("traffic_compact_opt1.3b-decode.json",
+                                             f"{w3.name}/steps{w3.decode_steps}"),
         "prefill_tflops_algorithmic": pf["achieved"], "prefill_frac_algorithmic": pf["frac"],
         "prefill_tflops_executed": pf["executed_tflops"],
         "decode_tokens_per_s": r["decode_tokens_per_s"], "timed_steps": a.steps}
