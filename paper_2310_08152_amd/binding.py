@@ -126,25 +126,44 @@ def _avail(t) -> int:
     return t.untyped_storage().nbytes() // t.element_size() - t.storage_offset()
 
 
+_torch = None
+
+
+def _tm():
+    """torch, imported on first use (host-only callers never need it)."""
+    global _torch, _I32, _FLOATS, _raw_stream
+    if _torch is None:
+        import torch
+        _I32, _FLOATS = torch.int32, (torch.float32, torch.bfloat16)
+        _raw_stream = torch._C._cuda_getCurrentRawStream
+        _torch = torch
+    return _torch
+
+
 def _dev(t, what, kind=None, need=0, contiguous=False, nullable=False):
     """Address of a device tensor after checking what the kernels will
     assume of it: on a GPU, of the element type `kind` ("i32", "float":
     fp32 or bf16, "u8": any byte workspace), contiguous if asked, and with
     at least `need` elements from its first one to the end of its storage
     (so no kernel addresses memory outside the allocation)."""
-    import torch
+    torch = _torch or _tm()
     if t is None:
         if nullable:
             return None
         _fail(f"{what}: missing (None)")
     if not isinstance(t, torch.Tensor) or not t.is_cuda:
         _fail(f"{what}: must be a device (cuda) tensor")
-    if kind == "i32" and t.dtype != torch.int32:
-        _fail(f"{what}: must be int32, got {t.dtype}")
-    if kind == "float" and t.dtype not in (torch.float32, torch.bfloat16):
-        _fail(f"{what}: must be float32 or bfloat16, got {t.dtype}")
-    if contiguous and not t.is_contiguous():
-        _fail(f"{what}: must be contiguous")
+    if kind is not None:
+        dt = t.dtype
+        if kind == "i32" and dt != _I32:
+            _fail(f"{what}: must be int32, got {dt}")
+        if kind == "float" and dt not in _FLOATS:
+            _fail(f"{what}: must be float32 or bfloat16, got {dt}")
+    if contiguous:
+        if not t.is_contiguous():
+            _fail(f"{what}: must be contiguous")
+        if need <= t.numel():  # a contiguous tensor holds its numel elements from the first
+            return t.data_ptr()
     if need > _avail(t):
         _fail(f"{what}: {need} elements addressed, only {_avail(t)} in its storage")
     return t.data_ptr()
@@ -153,10 +172,15 @@ def _dev(t, what, kind=None, need=0, contiguous=False, nullable=False):
 def _rows(t, what, b, H, n, d, stride_bh, dtype=None):
     """(b, H, n, d) slices with (b, h) stride stride_bh: rows contiguous,
     the batch stride H * stride_bh, element type as `dtype` (if given)."""
-    if t is not None and t.dim() == 4 and t.shape[0] == b and t.shape[1] == H:
-        if n > 1 and t.stride(2) != d or t.stride(3) != 1:
+    if t is not None and t.dim() == 4:
+        sh, st = t.shape, t.stride()
+        four = sh[0] == b and sh[1] == H
+    else:
+        four = False
+    if four:
+        if n > 1 and st[2] != d or st[3] != 1:
             _fail(f"{what}: rows of {d} elements must be contiguous")
-        if H > 1 and t.stride(1) != stride_bh or b > 1 and t.stride(0) != H * stride_bh:
+        if H > 1 and st[1] != stride_bh or b > 1 and st[0] != H * stride_bh:
             _fail(f"{what}: (b, h) slices must be stride_bh = {stride_bh} apart")
     elif t is not None and not t.is_contiguous():
         _fail(f"{what}: expected a (b, H, n, d) view or a contiguous tensor")
@@ -167,12 +191,14 @@ def _rows(t, what, b, H, n, d, stride_bh, dtype=None):
 
 
 def _stream(stream, *tensors):
+    """The caller's stream, else the current stream of the first device
+    tensor's GPU."""
     if stream is not None:
         return stream
-    import torch
+    torch = _torch or _tm()
     for t in tensors:
-        if t is not None and hasattr(t, "is_cuda") and t.is_cuda:
-            return torch.cuda.current_stream(t.device).cuda_stream
+        if isinstance(t, torch.Tensor) and t.is_cuda:
+            return _raw_stream(t.get_device())
     return None
 
 

@@ -316,6 +316,12 @@ __device__ __forceinline__ void prefill_attn_body(
   // with padding, V^T row D is all ones, so the PV MFMA also produces each
   // query's probability sum (O^T row D) and no separate row sum is needed.
   constexpr bool ONES_SUM = BF && (C::DP != D);
+  // Without padding (bf16, D = 64) the sums come from a 16x16x32 MFMA of the
+  // probabilities against a 0/1 matrix: lane L's A operand is all ones when
+  // bit 2 of L equals bit 4 of L, so D[4*(L/16) + j][L%16] adds the two
+  // lanes that hold query L%32's probabilities (lanes q and q + 32 of the
+  // 32x32x16 B operand), and every lane receives its own query's sum.
+  constexpr bool MFMA_SUM = BF && !ONES_SUM;
   if constexpr (C::DP != D) {
     for (int b = 0; b < C::NBUF; ++b) {
       char* vbuf = b == 0 ? vbuf0 : vbuf1;
@@ -370,6 +376,7 @@ __device__ __forceinline__ void prefill_attn_body(
 #pragma unroll
     for (int i = 0; i < 16; ++i) oacc[db][i] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
+  f32x4 lacc = {0.f, 0.f, 0.f, 0.f};
 
   // ---- staging: list entries run two tiles ahead through an LDS ring; the
   // key/value rows of tile kt+1 go global -> LDS by direct loads addressed
@@ -568,7 +575,8 @@ __device__ __forceinline__ void prefill_attn_body(
         if (__ballot(grow) != 0) {
           const float alpha = grow ? fast_exp2(m_run - mx) : 1.f;  // m_run == -inf gives 0
           if (grow) m_run = mx;
-          l_run *= alpha;
+          if constexpr (MFMA_SUM) lacc *= alpha;
+          else l_run *= alpha;
 #pragma unroll
           for (int db = 0; db < NDB; ++db)
 #pragma unroll
@@ -582,9 +590,9 @@ __device__ __forceinline__ void prefill_attn_body(
           for (int vv = 0; vv < 16; ++vv) {
             const float p = fast_exp2(fmaf(sacc[kb][vv], c2, -m_use));
             sacc[kb][vv] = p;
-            if constexpr (!ONES_SUM) rs += p;
+            if constexpr (!ONES_SUM && !MFMA_SUM) rs += p;
           }
-        if constexpr (!ONES_SUM) l_run += rs;
+        if constexpr (!ONES_SUM && !MFMA_SUM) l_run += rs;
         // ---- O^T += V^T P^T over the step's keys, 16 at a time ----
         if constexpr (BF) {
           bf16x8 pb[2 * NB];
@@ -595,6 +603,14 @@ __device__ __forceinline__ void prefill_attn_body(
             for (int i = 0; i < 4; ++i)
               w[i] = pack_bf16x2(sacc[tt >> 1][8 * (tt & 1) + 2 * i], sacc[tt >> 1][8 * (tt & 1) + 2 * i + 1]);
             pb[tt] = __builtin_bit_cast(bf16x8, w);
+          }
+          if constexpr (MFMA_SUM) {
+            const int ln = threadIdx.x & 63;
+            const uint32_t one = (((ln >> 2) ^ (ln >> 4)) & 1) ? 0u : 0x3f803f80u;
+            const bf16x8 ones_a = __builtin_bit_cast(bf16x8, u32x4{one, one, one, one});
+#pragma unroll
+            for (int tt = 0; tt < 2 * NB; ++tt)
+              lacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones_a, pb[tt], lacc, 0, 0, 0);
           }
           const uint16_t* vs = reinterpret_cast<const uint16_t*>(vcur);
 #pragma unroll
@@ -676,6 +692,8 @@ __device__ __forceinline__ void prefill_attn_body(
     // O^T row D sits in d-block D/32, accumulator 8*((D%32)/8) of lane group 0
     static_assert((D % 32) % 8 == 0, "ones row must start a group of 8 rows");
     l_tot = __shfl(oacc[D / 32][4 * ((D % 32) / 8)], l32, 64);
+  } else if constexpr (MFMA_SUM) {
+    l_tot = lacc[0];
   } else {
     l_tot = l_run + __shfl_xor(l_run, 32, 64);
   }

@@ -51,12 +51,16 @@ class KVCache:
         self.kept_src = torch.empty(b, L_cap, dtype=torch.int32, device=device)
         self.cur_tok = torch.zeros(b, dtype=torch.int32, device=device)
         self.status = torch.zeros(1, dtype=torch.int32, device=device)
+        # per-layer views, made once: indexing a tensor costs microseconds of
+        # host time, and decode issues one call per layer per token
+        self._k = [self.kv[m, 0] for m in range(M)]
+        self._v = [self.kv[m, 1] for m in range(M)]
 
     def k(self, m: int):
-        return self.kv[m, 0]
+        return self._k[m]
 
     def v(self, m: int):
-        return self.kv[m, 1]
+        return self._v[m]
 
     def start_prompt(self, L: int, meta: SpanMeta):
         """Rows [0, L) hold prompt tokens 0..L-1; the next token is L."""

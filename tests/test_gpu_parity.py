@@ -634,3 +634,15 @@ def test_binding_rejects_bad_device_tensors():
         B.span_masked_prefill_attn(x, x, x, x.clone(), b, H, L, d, L * d, 2 * L * d, L * d, 0.125,
                                    vu, T, pws)
     torch.cuda.synchronize()
+
+
+def test_binding_launches_on_the_current_stream():
+    """Without an explicit stream the calls go to torch's current stream of
+    the tensors' GPU, also inside a `torch.cuda.stream` block."""
+    B = P().B
+    x = torch.zeros(4, device=DEV)
+    assert B._stream(None, x) == torch.cuda.current_stream(x.device).cuda_stream
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        assert B._stream(None, x) == s.cuda_stream
+    assert B._stream(None, x) == torch.cuda.current_stream(x.device).cuda_stream
