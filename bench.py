@@ -783,6 +783,8 @@ def measure(args, w):
         out["prefill_block"] = pb
         out["roofline_prefill"]["kernel"] = ("prompt phase per layer, block-wise: rope_apply_at + "
                                              "span_masked_prefill_attn_cached + kv_compact")
+        # the stored counter figures are the one-shot kernel's, not this phase's
+        out["roofline_prefill"]["traffic"] = out["roofline_prefill"]["mfma_busy"] = None
         out["phases_ms"]["prompt_blockwise"] = out["phases_ms"].pop("rope+prefill")
         out["phases_ms"].pop("compaction", None)
         out["compaction_gbs"] = out["compaction_bytes"] = out["compaction_traffic"] = None
