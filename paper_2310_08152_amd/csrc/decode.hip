@@ -34,12 +34,38 @@ namespace sckv {
 //    about DEC_CH rows, one 4-wave workgroup each, and a second kernel merges
 //    the chunk partials.
 //  * Otherwise one workgroup per slice writes the output itself (no second
-//    launch): 4 waves (bf16) or 512 threads (fp32) below DEC_NARROW_MIN
-//    slices, and from there on 2 waves (bf16) or 256 threads (fp32), which
-//    keeps more workgroups resident per CU.
+//    launch).  fp32: 512 threads below DEC_NARROW_MIN slices, 256 from there
+//    on.  bf16: the most waves per slice (4, 2 or 1; 1 only where d <= 64)
+//    with which every wave of the launch is resident at once (the kernel
+//    holds two waves per SIMD), so the launch runs in one round; where even
+//    one wave per slice exceeds that, 4 waves, whose shorter workgroups
+//    balance the rounds best.  Measured: 512 slices (d=80) 4 waves; 2048
+//    slices (d=64) 1 wave 2% faster than 2 and 4% faster than 4; 8192
+//    slices (d=80) 4 waves 2.5% faster than 2.
 constexpr int DEC_CH = 1024;
 constexpr int DEC_SINGLE_MIN = 512;
 constexpr int DEC_NARROW_MIN = 1024;
+constexpr int DEC_WAVES_PER_SIMD = 2;  // decode_mfma_kernel's occupancy (its register count)
+
+// compute units of the current device, asked once per device
+static int device_cus(int* cus) {
+  static std::mutex mu;
+  static int cached[64] = {0};
+  int dev = 0;
+  int rc = hip_check(hipGetDevice(&dev), "compacted_decode_attn: hipGetDevice");
+  if (rc) return rc;
+  if (dev < 0 || dev >= 64) return fail(SCKV_EUNSUP, "compacted_decode_attn: device index above 63");
+  std::lock_guard<std::mutex> lock(mu);
+  if (cached[dev] == 0) {
+    int n = 0;
+    rc = hip_check(hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev),
+                   "compacted_decode_attn: hipDeviceGetAttribute");
+    if (rc) return rc;
+    cached[dev] = n > 0 ? n : 1;
+  }
+  *cus = cached[dev];
+  return 0;
+}
 constexpr int DEC_THREADS = 256;  // fp32 split chunks
 constexpr float LOG2E = 1.4426950408889634f;
 
@@ -751,7 +777,19 @@ static int launch_decode(const void* q, const void* k_new, const void* v_new, vo
   if (slices >= DEC_SINGLE_MIN) {
     const bool narrow = slices >= DEC_NARROW_MIN;
     if constexpr (sizeof(T) == 2) {
-      if (narrow)
+      int cus = 0;
+      const int rc = device_cus(&cus);
+      if (rc) return rc;
+      const int64_t slots = (int64_t)cus * 4 * DEC_WAVES_PER_SIMD;  // resident waves
+      const int nw = (int64_t)slices * 4 <= slots   ? 4
+                     : (int64_t)slices * 2 <= slots ? 2
+                     : slices <= slots              ? (D <= 64 ? 1 : 2)
+                                                    : 4;
+      if (nw == 1)  // D <= 64 here; the instantiation for larger D is never launched
+        decode_mfma_kernel<(D <= 64 ? D : 64), 1, true><<<slices, 64, 0, stream>>>(
+            qq, kn, vn, kc, vc, kv_len, cur_tok, vu, pos, L_meta, H, L_cap, qs, rotate, tab, part,
+            1, slices, L_cap, out, status, ring);
+      else if (nw == 2)
         decode_mfma_kernel<D, 2, true><<<slices, 128, 0, stream>>>(
             qq, kn, vn, kc, vc, kv_len, cur_tok, vu, pos, L_meta, H, L_cap, qs, rotate, tab, part,
             1, slices, L_cap, out, status, ring);
