@@ -368,12 +368,16 @@ def test_compaction_incremental_equals_one_shot():
 # ---------------------------------------------------------------------------
 
 # The launch shape follows the number of (sequence, head) slices: H=3 gives
-# 24 slices, split into chunks merged by a second kernel; H=64 gives 512
-# slices and H=128 gives 1024, one workgroup each (wide, then narrow).
+# 24 slices, split into chunks merged by a second kernel; from H=64 (512
+# slices) on, one workgroup per slice: bf16 with 4 waves at 512 slices, 2 at
+# 1024, 1 (d=64) or 2 (d=80) at 2048 (H=256), and 4 again at 4096 (H=512),
+# past what one round of the chip holds; fp32 512 or 256 threads.
 @pytest.mark.parametrize("dtype,d,theta,H", [("bf16", 64, 0.0, 3), ("bf16", 80, 10000.0, 3),
                                              ("f32", 64, 0.0, 3), ("f32", 80, 10000.0, 3),
                                              ("bf16", 80, 10000.0, 64), ("f32", 64, 0.0, 64),
-                                             ("bf16", 64, 0.0, 128), ("f32", 80, 10000.0, 128)])
+                                             ("bf16", 64, 0.0, 128), ("f32", 80, 10000.0, 128),
+                                             ("bf16", 64, 10000.0, 256), ("bf16", 80, 10000.0, 256),
+                                             ("bf16", 64, 0.0, 512)])
 def test_decode_matches_oracle(dtype, d, theta, H):
     say(f"decode dtype={dtype} d={d} theta={theta} H={H}")
     L_cap = 700
@@ -419,12 +423,13 @@ def test_decode_matches_oracle(dtype, d, theta, H):
             assert torch.equal(cache.kv[:, :, s, :, :n], before[:, :, s, :, :n])
 
 
-@pytest.mark.parametrize("dtype,H", [("bf16", 3), ("bf16", 64), ("bf16", 128), ("f32", 64)])
-def test_decode_ignores_rows_past_the_slice(dtype, H):
+@pytest.mark.parametrize("dtype,H,d", [("bf16", 3, 80), ("bf16", 64, 80), ("bf16", 128, 80),
+                                       ("f32", 64, 80), ("bf16", 256, 64)])
+def test_decode_ignores_rows_past_the_slice(dtype, H, d):
     """Rows at or past kv_len may hold anything (never written, or NaN/Inf
     bit patterns): the output over short and long slices must not change."""
-    say(f"decode past-the-slice rows dtype={dtype} H={H}")
-    L_cap, d = 600, 80
+    say(f"decode past-the-slice rows dtype={dtype} H={H} d={d}")
+    L_cap = 600
     lens = [0, 1, 31, 37, 100, 255, 256, 599]
     b = len(lens)
     meta = P().SpanMeta([[] for _ in range(b)], 1000, DEV)
