@@ -126,7 +126,7 @@ def _avail(t) -> int:
     return t.untyped_storage().nbytes() // t.element_size() - t.storage_offset()
 
 
-_torch = None
+_torch = _I32 = _FLOATS = _raw_stream = None
 
 
 def _tm():
@@ -135,7 +135,10 @@ def _tm():
     if _torch is None:
         import torch
         _I32, _FLOATS = torch.int32, (torch.float32, torch.bfloat16)
-        _raw_stream = torch._C._cuda_getCurrentRawStream
+        # the raw handle of the current stream of a device, without building
+        # a Stream object per call
+        _raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None) or (
+            lambda dev: torch.cuda.current_stream(dev).cuda_stream)
         _torch = torch
     return _torch
 
