@@ -466,6 +466,7 @@ def extra_configs(args):
         "prefill_tflops_executed": pf["executed_tflops"],
         "frac_executed": round(pf["executed_tflops"] / BF16_PEAK_TFLOPS, 4),
         "executed_over_algorithmic": pf["executed_over_algorithmic"],
+        "floors_us": pf["floors_us"], "frac_of_roofline": pf["frac_of_roofline"],
         "avg_launch_us": pf["avg_launch_us"], "plan_us": pf["plan_us"],
         "traffic": stored_traffic("traffic_prefill_opt1.3b-prefill.json", f"{w2.name}/steps0"),
         "traffic_unit": "HBM bytes per call (rocprofv3 FETCH_SIZE + WRITE_SIZE, calibrated)",
@@ -688,6 +689,7 @@ def measure(args, w):
     dec_bytes_launch = dec_bytes_step / n_dec if n_dec else 0.0
     pf_tflops_exe = pf_exe / (pf_avg_ms * 1e-3) / 1e12
     pf_tflops_alg = pf_alg / (pf_avg_ms * 1e-3) / 1e12
+    pf_ref_bytes = 4 * b * H * L * d * (2 if w.dtype == "bf16" else 4)  # Q, K, V in, O out
     ms_per_step = float(np.mean(step_ms))
 
     # the library's launch shape: one workgroup per (sequence, head) slice from
@@ -737,6 +739,13 @@ def measure(args, w):
                              "unit": "TFLOP/s", "frac": round(pf_tflops_alg / BF16_PEAK_TFLOPS, 4),
                              "executed_tflops": round(pf_tflops_exe, 1),
                              "executed_over_algorithmic": round(pf_exe / pf_alg, 3),
+                             # the two roofline floors of one call: algorithmic flops at
+                             # the MFMA peak, Q, K, V read and O written once at the HBM peak
+                             "floors_us": {"mfma": round(pf_alg / BF16_PEAK_TFLOPS / 1e6, 1),
+                                           "hbm": round(pf_ref_bytes / HBM_PEAK_GBS / 1e3, 1)},
+                             "frac_of_roofline": round(max(pf_alg / BF16_PEAK_TFLOPS / 1e6,
+                                                           pf_ref_bytes / HBM_PEAK_GBS / 1e3)
+                                                       / (pf_avg_ms * 1e3), 4),
                              "avg_launch_us": round(pf_avg_ms * 1e3, 1),
                              "plan_us": None if plan_ms is None else round(plan_ms * 1e3, 1),
                              "traffic": None if pf_traffic is None else int(pf_traffic),
