@@ -548,6 +548,67 @@ def test_end_to_end_prompt_compact_decode(case):
             assert np.array_equal(cache.pos_ids[s, :fin[4]].cpu().numpy(), fin[3][:fin[4]])
 
 
+def _pipeline_outputs(q, k, v, spans, L, steps, theta):
+    """Prompt, compaction and decode steps (compaction after each <CR>) on
+    the current stream; returns every output and the final bookkeeping."""
+    M, b, H, T, d = q.shape
+    meta = P().SpanMeta(spans, T, DEV)
+    cache = P().KVCache(M, b, H, T, d, q.dtype, DEV)
+    ws = P().Workspace(b, H, L, T, d, DEV)
+    cache.start_prompt(L, meta)
+    cr_steps = {r for sp in spans for _, r in sp if L <= r < T}
+    outs = []
+    P().prefill_plan(meta, ws, b, L)
+    for m in range(M):
+        qr = torch.empty(b, H, L, d, dtype=q.dtype, device=DEV)
+        P().rope_rows(q[m, :, :, :L], qr, meta, L, 0, theta)
+        P().rope_rows(k[m, :, :, :L], cache.k(m), meta, L, 0, theta)
+        P().rope_rows(v[m, :, :, :L], cache.v(m), meta, L, 0, 0.0)
+        o = torch.empty_like(qr)
+        P().prefill_layer(qr, cache.k(m), cache.v(m), o, meta, ws, L, planned=True)
+        outs.append(o)
+    cache.compact(meta)
+    for t in range(L, L + steps):
+        for m in range(M):
+            od = torch.empty(b, H, d, dtype=q.dtype, device=DEV)
+            P().decode_layer(q[m, :, :, t].contiguous(), k[m, :, :, t].contiguous(),
+                             v[m, :, :, t].contiguous(), cache, m, meta, ws, od, theta=theta)
+            outs.append(od)
+        cache.commit(meta)
+        if t in cr_steps:
+            cache.compact(meta)
+    return outs, cache
+
+
+def test_pipeline_on_a_side_stream_is_bitexact():
+    """The whole path launched inside `torch.cuda.stream(s)` (every call on
+    that stream, no explicit stream argument) gives the same bytes as on the
+    default stream."""
+    say("pipeline on a side stream")
+    M, b, H, L, steps, d, theta = 2, 2, 4, 300, 20, 80, 10000.0
+    T = L + steps
+    rng = np.random.default_rng(17)
+    spans = [random_spans(L, rng, max_len=30) + [(L + 3, L + 9)] for _ in range(b)]
+    q, k, v = (rnd((M, b, H, T, d), 400 + i, "bf16") for i in range(3))
+    torch.cuda.synchronize()
+    ref, ref_cache = _pipeline_outputs(q, k, v, spans, L, steps, theta)
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        got, got_cache = _pipeline_outputs(q, k, v, spans, L, steps, theta)
+    s.synchronize()
+    assert int(ref_cache.status) == 0 and int(got_cache.status) == 0
+    for a, c in zip(ref, got):
+        assert torch.equal(a, c)
+    assert torch.equal(ref_cache.kv_len, got_cache.kv_len)
+    for i in range(b):  # rows past a sequence's length were never written
+        n = int(ref_cache.kv_len[i])
+        assert torch.equal(ref_cache.kv[:, :, i, :, :n], got_cache.kv[:, :, i, :, :n])
+        assert torch.equal(ref_cache.tok_idx[i, :n], got_cache.tok_idx[i, :n])
+        assert torch.equal(ref_cache.pos_ids[i, :n], got_cache.pos_ids[i, :n])
+
+
 # ---------------------------------------------------------------------------
 # local-attention comparator: ring of the W most recent tokens
 # ---------------------------------------------------------------------------
