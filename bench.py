@@ -97,7 +97,9 @@ def last_visible_row(spans, L):
 def prefill_work(spans_all, L, H, d):
     """(algorithmic flops, executed flops) of one layer's prefill: 4*d per
     visible (row, column) pair, and 4*d per pair of every 32x64 tile a wave
-    multiplies."""
+    multiplies (at d=64 the kernel skips a tile's second 32-key block where
+    it lies past the list's end or starts after the wave's last row, and such
+    a tile counts 32x32)."""
     alg = 0
     exe = 0
     for spans in spans_all:
@@ -120,7 +122,14 @@ def prefill_work(spans_all, L, H, d):
                 if Iw >= L:
                     continue
                 jmin = cols[::PF_BK][:nt]
-                exe += int((jmin <= Iw + 31).sum()) * PF_BK * 32
+                done = jmin <= Iw + 31
+                exe += int(done.sum()) * PF_BK * 32
+                if d == 64 and nt:
+                    second = np.arange(nt) * PF_BK + 32  # list index of each tile's second block
+                    has2 = second < len(cols)
+                    j32 = cols[np.minimum(second, len(cols) - 1)]
+                    skip2 = ~has2 | (j32 > Iw + 31)
+                    exe -= int((done & skip2).sum()) * 32 * 32
     return 4 * d * alg * H, 4 * d * exe * H
 
 

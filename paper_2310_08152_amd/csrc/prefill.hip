@@ -525,8 +525,18 @@ __device__ __forceinline__ void prefill_attn_body(
     const uint32_t* tent = ent_ring[kt % PF_ER];
     if (wave_live && ti.jmin <= Iw + 31) {
       const bool full = ti.nvalid == PF_BK && ti.jmax <= Iw && ti.vrmin >= Iw + 31 - I;
+      // With one 32-key block per step, the second block is skipped where
+      // no row of this wave can see any of it: it lies past the list's end,
+      // or (the list being in token order) its first token is later than the
+      // wave's last row.
+      bool skip2 = false;
+      if constexpr (NB == 1) {
+        const int j32 = __builtin_amdgcn_readfirstlane((int)(tent[32] & 0x00ffffffu));
+        skip2 = ti.nvalid <= 32 || j32 > Iw + 31;
+      }
 #pragma unroll
       for (int st = 0; st < 2 / NB; ++st) {
+        if (st == 1 && skip2) break;
         // ---- S^T = K Q^T for the step's key blocks, key step outer so that
         // consecutive matrix instructions write different accumulators ----
         f32x16 sacc[NB];

@@ -35,6 +35,37 @@ def test_algorithmic_pairs_equal_oracle_mask(L, ratio, seed, open_tail):
     assert exe >= alg
 
 
+@pytest.mark.parametrize("L,ratio,seed,open_tail", [(200, 0.5, 2, False), (257, 0.8, 3, True),
+                                                    (600, 0.9, 11, False), (130, 0.0, 4, False)])
+def test_skipped_key_blocks_hold_no_visible_pair(L, ratio, seed, open_tail):
+    """At d=64 the kernel skips a tile's second 32-key block where it lies past
+    the block's list or starts after the wave's last row.  Against the
+    oracle's mask: no skipped block holds a pair its wave's rows can see, and
+    the executed count stays at or above the algorithmic one."""
+    spans = random_spans(L, ratio, seed, open_tail)
+    mask = O.attention_mask(O.token_types(spans, L))
+    vu = bench.last_visible_row(spans, L)
+    skipped = 0
+    for I in range(0, L, bench.PF_BQ):
+        cols = np.nonzero(vu[:min(I + bench.PF_BQ, L)] >= I)[0]
+        for w in range(4):
+            Iw = I + 32 * w
+            if Iw >= L:
+                continue
+            rows = slice(Iw, min(Iw + 32, L))
+            for t0 in range(0, len(cols), bench.PF_BK):
+                if cols[t0] > Iw + 31:
+                    continue  # the whole tile is skipped
+                half = cols[t0 + 32:t0 + bench.PF_BK]
+                if len(half) == 0 or half[0] > Iw + 31:
+                    assert not mask[rows][:, half].any()
+                    skipped += 1
+    alg, exe = bench.prefill_work([spans], L, 1, 64)
+    assert exe >= alg
+    _, exe80 = bench.prefill_work([spans], L, 1, 80)
+    assert exe80 // 80 - exe // 64 == 4 * 32 * 32 * skipped
+
+
 @pytest.mark.parametrize("L,ratio,seed", [(64, 0.3, 5), (300, 0.6, 6), (513, 0.9, 7)])
 def test_kept_rows_equal_oracle_keep_flags(L, ratio, seed):
     spans = random_spans(L, ratio, seed)
