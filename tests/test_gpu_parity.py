@@ -167,6 +167,10 @@ PREFILL_CASES = [
     ("bf16-d64-L37-zero-start", "bf16", 1, 3, 37, 64, "zero"),
     ("bf16-d80-L129-open", "bf16", 2, 1, 129, 80, "open"),
     ("bf16-d64-long-spans", "bf16", 1, 2, 700, 64, "long"),
+    # (sequence, head) slices are dispatched in groups of 8: a full group and a
+    # partial one, with an odd head count
+    ("bf16-d80-12-slices", "bf16", 3, 4, 600, 80, "uniform"),
+    ("bf16-d64-20-slices", "bf16", 4, 5, 513, 64, "random"),
 ]
 
 
