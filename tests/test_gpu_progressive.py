@@ -71,6 +71,8 @@ CASES = [
     ("f32-d64-rope-block64", "f32", 1, 2, 2, 300, 64, 1e4, 64, "random"),
     ("f32-d80-one-block", "f32", 1, 1, 2, 300, 80, 0.0, 300, "random"),
     ("bf16-d80-rope-block96-long-spans", "bf16", 1, 1, 2, 700, 80, 1e4, 96, "long"),
+    # a full and a partial 8-slice dispatch group (13 slices)
+    ("bf16-d64-block256-13-slices", "bf16", 1, 1, 13, 700, 64, 0.0, 256, "uniform"),
 ]
 
 
