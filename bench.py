@@ -43,6 +43,7 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, published
+F32_PEAK_TFLOPS = 157.3        # MI355X dense fp32 MFMA, published
 PF_BQ, PF_BK = 128, 64         # prefill query block / gathered key tile
 
 
@@ -473,7 +474,7 @@ def extra_configs(args):
                     f"d={w2.d_head}, L={w2.seq_len}, {r['config']['evicted']:.0%} freed",
         "prefill_tflops_algorithmic": pf["achieved"], "frac_algorithmic": pf["frac"],
         "prefill_tflops_executed": pf["executed_tflops"],
-        "frac_executed": round(pf["executed_tflops"] / BF16_PEAK_TFLOPS, 4),
+        "frac_executed": round(pf["executed_tflops"] / pf["peak"], 4),
         "executed_over_algorithmic": pf["executed_over_algorithmic"],
         "floors_us": pf["floors_us"], "frac_of_roofline": pf["frac_of_roofline"],
         "avg_launch_us": pf["avg_launch_us"], "plan_us": pf["plan_us"],
@@ -698,6 +699,7 @@ def measure(args, w):
     dec_bytes_launch = dec_bytes_step / n_dec if n_dec else 0.0
     pf_tflops_exe = pf_exe / (pf_avg_ms * 1e-3) / 1e12
     pf_tflops_alg = pf_alg / (pf_avg_ms * 1e-3) / 1e12
+    mfma_peak = BF16_PEAK_TFLOPS if w.dtype == "bf16" else F32_PEAK_TFLOPS
     pf_ref_bytes = 4 * b * H * L * d * (2 if w.dtype == "bf16" else 4)  # Q, K, V in, O out
     ms_per_step = float(np.mean(step_ms))
 
@@ -744,15 +746,15 @@ def measure(args, w):
         "roofline_prefill": {"bound": "mfma",
                              "kernel": "prefill_attn_kernel (span_masked_prefill_attn_planned; "
                                        "the plan kernel runs once per prompt, plan_us)",
-                             "achieved": round(pf_tflops_alg, 1), "peak": BF16_PEAK_TFLOPS,
-                             "unit": "TFLOP/s", "frac": round(pf_tflops_alg / BF16_PEAK_TFLOPS, 4),
+                             "achieved": round(pf_tflops_alg, 1), "peak": mfma_peak,
+                             "unit": "TFLOP/s", "frac": round(pf_tflops_alg / mfma_peak, 4),
                              "executed_tflops": round(pf_tflops_exe, 1),
                              "executed_over_algorithmic": round(pf_exe / pf_alg, 3),
                              # the two roofline floors of one call: algorithmic flops at
                              # the MFMA peak, Q, K, V read and O written once at the HBM peak
-                             "floors_us": {"mfma": round(pf_alg / BF16_PEAK_TFLOPS / 1e6, 1),
+                             "floors_us": {"mfma": round(pf_alg / mfma_peak / 1e6, 1),
                                            "hbm": round(pf_ref_bytes / HBM_PEAK_GBS / 1e3, 1)},
-                             "frac_of_roofline": round(max(pf_alg / BF16_PEAK_TFLOPS / 1e6,
+                             "frac_of_roofline": round(max(pf_alg / mfma_peak / 1e6,
                                                            pf_ref_bytes / HBM_PEAK_GBS / 1e3)
                                                        / (pf_avg_ms * 1e3), 4),
                              "avg_launch_us": round(pf_avg_ms * 1e3, 1),
