@@ -46,6 +46,7 @@ constexpr int DEC_CH = 1024;
 constexpr int DEC_SINGLE_MIN = 512;
 constexpr int DEC_NARROW_MIN = 1024;
 constexpr int DEC_WAVES_PER_SIMD = 2;  // decode_mfma_kernel's occupancy (its register count)
+constexpr int DEC_SPEC2_ROWS = 512;    // cache rows per wave from which two blocks are speculated
 
 // compute units of the current device, asked once per device
 static int device_cus(int* cus) {
@@ -457,7 +458,7 @@ constexpr int half_wave_count() {
   else return half_wave_count<NV, MASK / 2>();
 }
 
-template <int D, int NW, bool FINAL>
+template <int D, int NW, bool FINAL, bool SPEC2 = false>
 __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k_new,
     const uint16_t* __restrict__ v_new, uint16_t* __restrict__ k_cache,
@@ -521,6 +522,9 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
   };
   u32x4 kA[KS], vA[KS], kB[KS], vB[KS];
   if constexpr (FINAL) load_row(min(32 * wave + kr, L_cap - 1), kA, vA);
+  // with SPEC2 (chosen by the host for caches large enough that slices are
+  // taken to be long) the second block is issued before the length too
+  if constexpr (FINAL && SPEC2) load_row(min(32 * (wave + NW) + kr, L_cap - 1), kB, vB);
   const uint32_t* qw = reinterpret_cast<const uint32_t*>(q + (int64_t)bh * D);
   uint32_t qword[HD];
 #pragma unroll
@@ -547,7 +551,7 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
   // issued whether or not the wave has these blocks, so that the counter
   // waits below stay exact on every path
   if constexpr (FINAL) {
-    load_blk(wave + NW, kB, vB);
+    if constexpr (!SPEC2) load_blk(wave + NW, kB, vB);
     // a short slice: rows past its end were read too.  Their scores are
     // masked; their values are zeroed so that whatever those rows hold
     // (they may never have been written) adds exactly nothing.
@@ -555,6 +559,13 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
       const bool a_in = 32 * wave + kr < rc;
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) vA[kk] = a_in ? vA[kk] : u32x4{0, 0, 0, 0};
+    }
+    if constexpr (SPEC2) {
+      if (32 * (wave + NW) + 32 > rc) {
+        const bool b_in = 32 * (wave + NW) + kr < rc;
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk) vB[kk] = b_in ? vB[kk] : u32x4{0, 0, 0, 0};
+      }
     }
   } else {
     load_blk(wave, kA, vA);
@@ -785,18 +796,23 @@ static int launch_decode(const void* q, const void* k_new, const void* v_new, vo
                      : (int64_t)slices * 2 <= slots ? 2
                      : slices <= slots              ? (D <= 64 ? 1 : 2)
                                                     : 4;
-      if (nw == 1)  // D <= 64 here; the instantiation for larger D is never launched
-        decode_mfma_kernel<(D <= 64 ? D : 64), 1, true><<<slices, 64, 0, stream>>>(
-            qq, kn, vn, kc, vc, kv_len, cur_tok, vu, pos, L_meta, H, L_cap, qs, rotate, tab, part,
-            1, slices, L_cap, out, status, ring);
-      else if (nw == 2)
-        decode_mfma_kernel<D, 2, true><<<slices, 128, 0, stream>>>(
-            qq, kn, vn, kc, vc, kv_len, cur_tok, vu, pos, L_meta, H, L_cap, qs, rotate, tab, part,
-            1, slices, L_cap, out, status, ring);
-      else
-        decode_mfma_kernel<D, 4, true><<<slices, 256, 0, stream>>>(
-            qq, kn, vn, kc, vc, kv_len, cur_tok, vu, pos, L_meta, H, L_cap, qs, rotate, tab, part,
-            1, slices, L_cap, out, status, ring);
+      // A cache of at least DEC_SPEC2_ROWS rows per wave of a slice is taken
+      // to hold long slices: both first blocks of every wave are then read
+      // before the slice length arrives (rows past a shorter slice are read
+      // for nothing, never used).
+      const bool spec2 = ring == 0 && (int64_t)L_cap >= (int64_t)DEC_SPEC2_ROWS * nw;
+#define SCKV_DECODE_LAUNCH(DD, NWW, SP)                                                          \
+  decode_mfma_kernel<DD, NWW, true, SP><<<slices, NWW * 64, 0, stream>>>(                         \
+      qq, kn, vn, kc, vc, kv_len, cur_tok, vu, pos, L_meta, H, L_cap, qs, rotate, tab, part, 1,  \
+      slices, L_cap, out, status, ring)
+      constexpr int D1 = D <= 64 ? D : 64;  // nw == 1 only where D <= 64
+      if (nw == 1 && spec2) SCKV_DECODE_LAUNCH(D1, 1, true);
+      else if (nw == 1) SCKV_DECODE_LAUNCH(D1, 1, false);
+      else if (nw == 2 && spec2) SCKV_DECODE_LAUNCH(D, 2, true);
+      else if (nw == 2) SCKV_DECODE_LAUNCH(D, 2, false);
+      else if (spec2) SCKV_DECODE_LAUNCH(D, 4, true);
+      else SCKV_DECODE_LAUNCH(D, 4, false);
+#undef SCKV_DECODE_LAUNCH
     } else {
       if (narrow)
         decode_chunk_kernel<T, D, 256, true><<<slices, 256, 0, stream>>>(

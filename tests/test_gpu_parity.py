@@ -427,14 +427,17 @@ def test_decode_matches_oracle(dtype, d, theta, H):
             assert torch.equal(cache.kv[:, :, s, :, :n], before[:, :, s, :, :n])
 
 
-@pytest.mark.parametrize("dtype,H,d", [("bf16", 3, 80), ("bf16", 64, 80), ("bf16", 128, 80),
-                                       ("f32", 64, 80), ("bf16", 256, 64)])
-def test_decode_ignores_rows_past_the_slice(dtype, H, d):
+# A cache of at least 512 rows per wave of a slice has both first blocks of
+# every wave read before the slice length is known: L_cap=2100 at 4 waves and
+# L_cap=600 at one wave (H=256, d=64) read past the short slices too.
+@pytest.mark.parametrize("dtype,H,d,L_cap", [("bf16", 3, 80, 600), ("bf16", 64, 80, 600),
+                                             ("bf16", 128, 80, 600), ("f32", 64, 80, 600),
+                                             ("bf16", 256, 64, 600), ("bf16", 64, 80, 2100)])
+def test_decode_ignores_rows_past_the_slice(dtype, H, d, L_cap):
     """Rows at or past kv_len may hold anything (never written, or NaN/Inf
     bit patterns): the output over short and long slices must not change."""
-    say(f"decode past-the-slice rows dtype={dtype} H={H} d={d}")
-    L_cap = 600
-    lens = [0, 1, 31, 37, 100, 255, 256, 599]
+    say(f"decode past-the-slice rows dtype={dtype} H={H} d={d} L_cap={L_cap}")
+    lens = [0, 1, 31, 37, 100, 255, 256, L_cap - 1]
     b = len(lens)
     meta = P().SpanMeta([[] for _ in range(b)], 1000, DEV)
     cache = P().KVCache(1, b, H, L_cap, d, W().torch_dtype(dtype), DEV)
